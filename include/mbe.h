@@ -1,0 +1,173 @@
+/*
+ * mbe.h -- C ABI of libmbe: the editing-pass hot path of Multi-Block Editing
+ * (MBE) for block-diffusion language models, for AMD MI355X (gfx950).
+ *
+ * Paper: "Beyond Block Boundaries: Multi-Block Editing for Diffusion Large
+ * Language Models".
+ *
+ * Conventions shared by every call
+ *   - Every buffer argument is device memory owned by the caller.  The library
+ *     keeps no pointer after a call returns and allocates nothing.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream).  They never synchronise; results are valid once the stream has
+ *     been synchronised.
+ *   - Arguments are validated on the host before any HIP call.  A failed
+ *     check returns a non-OK status, launches nothing and writes nothing.
+ *     mbe_last_error() then holds a thread-local description.
+ *   - Per-sequence values that live in device memory (page ids, lengths) are
+ *     preconditions and are not read back.  Page ids outside [0, num_pages)
+ *     are clamped into range, so a bad table gives wrong numbers but never an
+ *     out-of-bounds access.  With the environment variable MBE_DEBUG_CHECK=1,
+ *     the attention calls copy the lengths and the page table to the host
+ *     (synchronously) and return MBE_ERR_BAD_VALUE on a violation.
+ *   - An error from the HIP runtime is returned as MBE_ERR_HIP, with the HIP
+ *     error string in mbe_last_error().
+ *   - No global mutable state except the thread-local error string.  Calls
+ *     that share a workspace must not overlap in time.
+ */
+#ifndef MBE_H_
+#define MBE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MBE_OK = 0,
+  MBE_ERR_NULL_ARG = 1,     /* a required pointer is NULL                      */
+  MBE_ERR_BAD_SHAPE = 2,    /* sizes inconsistent or negative                  */
+  MBE_ERR_UNSUPPORTED = 3,  /* head_dim, page size or mask mode not supported  */
+  MBE_ERR_WORKSPACE = 4,    /* workspace missing or smaller than required      */
+  MBE_ERR_HIP = 5,          /* HIP runtime or launch error                     */
+  MBE_ERR_BAD_VALUE = 6     /* bad scalar (NaN threshold) or, under
+                               MBE_DEBUG_CHECK=1, a bad per-sequence value     */
+} mbe_status;
+
+/* Attention scope of the window queries.
+ *   MBE_MASK_WINDOW_BIDIR: every prefix token and every window token is
+ *     visible.  This is the MBE editing pass, with full attention within the
+ *     window W_j = [j*B, (j+1)B) (paper, Sec. "Training-Free MBE Decoding",
+ *     Eq. (4)).
+ *   MBE_MASK_BLOCK_CAUSAL: every prefix token and the window blocks up to the
+ *     query's own block are visible.  This is the standard block-diffusion
+ *     scope (Sec. "Block diffusion") that refresh recomputes use.
+ * The two coincide when the window is one block. */
+typedef enum { MBE_MASK_WINDOW_BIDIR = 0, MBE_MASK_BLOCK_CAUSAL = 1 } mbe_mask_mode;
+
+/* Paged KV cache for one layer.  Pages hold 16 tokens; all bf16.
+ *   k_pages: [num_pages][num_kv_heads][16][head_dim]   token-major page
+ *   v_pages: [num_pages][num_kv_heads][head_dim][16]   token-minor page
+ * Token t of sequence b is slot t % 16 of page page_table[b][t / 16].  The
+ * window's own K/V (tokens P_b .. P_b+W_b-1) are read through the same table
+ * from pages the caller provides.  The library only reads the cache, as the
+ * paper's cache control requires (Sec. "Infrastructure Optimization").
+ * The bytes of token slots that no sequence covers (the tail of a sequence's
+ * last page) are never used and may hold anything, NaN included. */
+typedef struct {
+  const void *k_pages;
+  const void *v_pages;
+  int32_t num_pages;
+  int32_t page_size;     /* must be 16            */
+  int32_t num_kv_heads;  /* Hkv >= 1              */
+  int32_t head_dim;      /* D: 64 or 128          */
+} mbe_paged_kv;
+
+/* Options of the attention calls.  The bounds are host-side facts the caller
+ * knows without reading device memory.  They size the grid and the
+ * workspace; the kernels read the true lengths from device memory. */
+typedef struct {
+  int32_t batch;              /* number of sequences, >= 0                          */
+  int32_t num_q_heads;        /* Hq, a multiple of num_kv_heads                      */
+  int32_t max_pages_per_seq;  /* row length of page_table                           */
+  int32_t total_q;            /* rows of q/out = sum of window lengths               */
+  int32_t max_prefix_len;     /* >= every P_b                                        */
+  int32_t max_window_len;     /* >= every W_b; a multiple of block_size              */
+  int32_t mask_mode;          /* mbe_mask_mode                                      */
+  float softmax_scale;        /* <= 0 selects 1/sqrt(head_dim)                      */
+  int32_t kv_split_tokens;    /* keys per split-KV chunk; 0 lets the library choose;
+                                 otherwise a positive multiple of 64                 */
+  void *workspace;            /* device memory of mbe_window_attention_workspace_size
+                                 bytes, 256-byte aligned, zero-filled before its first
+                                 use (see mbe_workspace_zero).  Its first 64 KB hold
+                                 arrival counters that every call leaves at zero;
+                                 results go after them, so one workspace serves calls
+                                 of any shape that fit in it                         */
+  size_t workspace_bytes;
+  void *stream;               /* hipStream_t                                        */
+} mbe_attn_opts;
+
+/* Editing-window attention (paper, Sec. "Training-Free MBE Decoding", Eq. (4)).
+ *   q:           bf16 [total_q][Hq][D]; the W_b rows of sequence b start at row
+ *                sum_{b' < b} W_b' and row i is window position P_b + i.
+ *   paged_kv:    the cache, see mbe_paged_kv.
+ *   page_table:  int32 [batch][max_pages_per_seq]; must cover P_b + W_b tokens.
+ *   prefix_lens: int32 [batch], P_b >= 0 committed prefix tokens.
+ *   window_lens: int32 [batch], W_b >= 0, a multiple of block_size.
+ *   block_size:  B >= 1.
+ *   out:         bf16 [total_q][Hq][D], written for every row.
+ * Query head h reads KV head h / (Hq / Hkv).  The scale is applied to q.k
+ * before a softmax over the visible keys (fp32 accumulation).
+ * Returns MBE_OK with no launch when batch or total_q is 0. */
+mbe_status mbe_window_attention(const void *q, const mbe_paged_kv *paged_kv,
+                                const int32_t *page_table, const int32_t *prefix_lens,
+                                const int32_t *window_lens, int32_t block_size, void *out,
+                                const mbe_attn_opts *opts);
+
+/* Standard single-block block-diffusion attention (paper, Sec. "Block
+ * diffusion"): each sequence's B = block_size queries attend to its prefix
+ * and bidirectionally to their own block.  This is mbe_window_attention with
+ * W_b = block_size for every b; opts->max_window_len and opts->mask_mode are
+ * ignored, and opts->total_q must equal batch * block_size. */
+mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv,
+                                     const int32_t *page_table, const int32_t *prefix_lens,
+                                     int32_t block_size, void *out, const mbe_attn_opts *opts);
+
+/* Workspace bytes the attention calls need for these shapes and options:
+ * 64 KB of arrival counters (one per 256-row query tile, at most 16384 tiles
+ * when the key range is split) plus the split-KV partial results.  0 means
+ * the plan needs no split and no workspace.
+ * Returns (size_t)-1 if the arguments are invalid. */
+size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv,
+                                           const mbe_attn_opts *opts, int32_t block_size);
+
+/* Confidence-based edit selection (paper, Sec. "Configurable threshold
+ * decoding", Eq. (1), the token-to-token set), for every row r:
+ *   a       = lowest index v with logits[r][v] maximal
+ *   conf[r] = softmax probability of a = 1 / sum_v exp(logits[r][v] - logits[r][a])
+ *   changed = (a != cur_tokens[r]) && (conf[r] >= threshold)
+ *   new_tokens[r] = changed ? a : cur_tokens[r];  changed_mask[r] = changed
+ * logits: bf16 [rows][row_stride], row_stride >= vocab; -inf entries allowed;
+ * NaN or all -inf rows are outside the contract.  Accumulation is fp32; conf
+ * is a correctly rounded reciprocal.  Deterministic: the same inputs give
+ * bitwise the same outputs.  workspace: mbe_edit_select_workspace_size bytes,
+ * 256-byte aligned, zero-filled before first use; its first 64 KB are arrival
+ * counters that every call leaves at zero (may be NULL when the size is 0).
+ * Returns MBE_OK with no launch when rows is 0; MBE_ERR_BAD_VALUE for a NaN
+ * threshold. */
+mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                           const int32_t *cur_tokens, float threshold, int32_t *new_tokens,
+                           float *conf, uint8_t *changed_mask, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+/* Workspace bytes mbe_edit_select needs for rows x vocab (0 = none).
+ * Returns (size_t)-1 for negative sizes. */
+size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab);
+
+/* Zero-fills `bytes` bytes of a workspace on `stream` with a kernel (no
+ * hipMemset), e.g. once after allocating it. */
+mbe_status mbe_workspace_zero(void *workspace, size_t bytes, void *stream);
+
+/* Static description of a status code. */
+const char *mbe_status_string(mbe_status s);
+
+/* Thread-local detail of the last non-OK status returned on this thread. */
+const char *mbe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MBE_H_ */

@@ -1,0 +1,245 @@
+"""Python binding of libmbe, the MBE editing-pass hot path on MI355X (gfx950).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+libmbe.so, called through its C ABI (include/mbe.h) with ctypes.  PyTorch
+provides device memory and the current stream.  If libmbe.so is missing or
+cannot be loaded, every call raises; there is no other implementation.
+
+    window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size)
+    block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size)
+    edit_select(logits, cur_tokens, threshold) -> (new_tokens, conf, changed_mask)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmbe.so")
+
+MBE_OK = 0
+STATUS_NAMES = {0: "MBE_OK", 1: "MBE_ERR_NULL_ARG", 2: "MBE_ERR_BAD_SHAPE", 3: "MBE_ERR_UNSUPPORTED",
+                4: "MBE_ERR_WORKSPACE", 5: "MBE_ERR_HIP", 6: "MBE_ERR_BAD_VALUE"}
+MASK_MODES = {"bidir": 0, "block_causal": 1}
+
+EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
+           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_workspace_zero",
+           "mbe_status_string", "mbe_last_error")
+
+
+class MbeError(RuntimeError):
+    def __init__(self, call, status, detail):
+        self.status = status
+        super().__init__(f"{call}: {STATUS_NAMES.get(status, status)}: {detail}")
+
+
+class PagedKV(ctypes.Structure):
+    _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
+                ("num_pages", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+
+
+class AttnOpts(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("max_pages_per_seq", ctypes.c_int32), ("total_q", ctypes.c_int32),
+                ("max_prefix_len", ctypes.c_int32), ("max_window_len", ctypes.c_int32),
+                ("mask_mode", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("kv_split_tokens", ctypes.c_int32), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p)]
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Loads libmbe.so (once).  Raises if it is missing or lacks a symbol."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        p = path or LIB_PATH
+        if not os.path.exists(p):
+            raise RuntimeError(f"{p} not found: build it with `python -m paper_2607_22663_amd.build`")
+        lib = ctypes.CDLL(p)
+        for name in EXPORTS:
+            if not hasattr(lib, name):
+                raise RuntimeError(f"{p} does not export {name}")
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        lib.mbe_window_attention.argtypes = [vp, ctypes.POINTER(PagedKV), vp, vp, vp, i32, vp,
+                                             ctypes.POINTER(AttnOpts)]
+        lib.mbe_window_attention.restype = ctypes.c_int
+        lib.block_diffusion_attention.argtypes = [vp, ctypes.POINTER(PagedKV), vp, vp, i32, vp,
+                                                  ctypes.POINTER(AttnOpts)]
+        lib.block_diffusion_attention.restype = ctypes.c_int
+        lib.mbe_window_attention_workspace_size.argtypes = [ctypes.POINTER(PagedKV),
+                                                            ctypes.POINTER(AttnOpts), i32]
+        lib.mbe_window_attention_workspace_size.restype = sz
+        lib.mbe_edit_select.argtypes = [vp, i64, i64, i64, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]
+        lib.mbe_edit_select.restype = ctypes.c_int
+        lib.mbe_edit_select_workspace_size.argtypes = [i64, i64]
+        lib.mbe_edit_select_workspace_size.restype = sz
+        lib.mbe_workspace_zero.argtypes = [vp, sz, vp]
+        lib.mbe_workspace_zero.restype = ctypes.c_int
+        lib.mbe_status_string.argtypes = [ctypes.c_int]
+        lib.mbe_status_string.restype = ctypes.c_char_p
+        lib.mbe_last_error.argtypes = []
+        lib.mbe_last_error.restype = ctypes.c_char_p
+        _lib = lib
+        return lib
+
+
+def _check(call, status):
+    if status != MBE_OK:
+        raise MbeError(call, status, load().mbe_last_error().decode(errors="replace"))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t: torch.Tensor, name: str, dtype, device, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
+
+
+_workspaces = {}
+
+
+def _workspace(kind: str, device: torch.device, nbytes: int, stream) -> Optional[torch.Tensor]:
+    """Per-(kind, device) workspace, grown on demand and zero-filled by the
+    library when (re)allocated; every call leaves it ready for the next."""
+    if nbytes == 0:
+        return None
+    key = (kind, device.index)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        _check("mbe_workspace_zero", load().mbe_workspace_zero(_ptr(ws), nbytes, stream))
+        _workspaces[key] = ws
+    return ws
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out):
+    dev = q.device
+    _need(q, "q", torch.bfloat16, dev, 3)
+    _need(k_pages, "k_pages", torch.bfloat16, dev, 4)
+    _need(v_pages, "v_pages", torch.bfloat16, dev, 4)
+    _need(page_table, "page_table", torch.int32, dev, 2)
+    _need(prefix_lens, "prefix_lens", torch.int32, dev, 1)
+    n_pages, hkv, page, d = k_pages.shape
+    if tuple(v_pages.shape) != (n_pages, hkv, d, page):
+        raise ValueError(f"v_pages must be [num_pages, Hkv, D, 16] = {(n_pages, hkv, d, page)}, "
+                         f"got {tuple(v_pages.shape)}")
+    if q.shape[2] != d:
+        raise ValueError(f"q head_dim {q.shape[2]} != cache head_dim {d}")
+    if page_table.shape[0] != prefix_lens.shape[0]:
+        raise ValueError("page_table and prefix_lens disagree on the batch size")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need(out, "out", torch.bfloat16, dev, 3)
+        if out.shape != q.shape:
+            raise ValueError("out must have the shape of q")
+    kv = PagedKV(_ptr(k_pages), _ptr(v_pages), n_pages, page, hkv, d)
+    return kv, out
+
+
+def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size, *,
+                     out=None, mask_mode="bidir", softmax_scale=None, max_prefix_len=None,
+                     max_window_len=None, kv_split_tokens=0):
+    """MBE editing-window attention (paper, Sec. "Training-Free MBE Decoding",
+    Eq. (4)).  Layouts as in include/mbe.h.  max_prefix_len / max_window_len
+    are host-side bounds; when omitted they are read from the device tensors
+    (a synchronisation)."""
+    lib = load()
+    kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
+    _need(window_lens, "window_lens", torch.int32, q.device, 1)
+    batch = prefix_lens.shape[0]
+    if max_prefix_len is None:
+        max_prefix_len = int(prefix_lens.max().item()) if batch else 0
+    if max_window_len is None:
+        max_window_len = int(window_lens.max().item()) if batch else 0
+    stream = _stream(q.device)
+    opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
+                    int(max_window_len), MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode),
+                    float(softmax_scale or 0.0), int(kv_split_tokens), None, 0, stream)
+    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+    if need == ctypes.c_size_t(-1).value:
+        _check("mbe_window_attention", lib.mbe_window_attention(
+            None, ctypes.byref(kv), None, None, None, int(block_size), None, ctypes.byref(opts)))
+    ws = _workspace("attn", q.device, need, stream)
+    opts.workspace = _ptr(ws)
+    opts.workspace_bytes = need
+    _check("mbe_window_attention", lib.mbe_window_attention(
+        _ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens), _ptr(window_lens),
+        int(block_size), _ptr(out), ctypes.byref(opts)))
+    return out
+
+
+def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size, *,
+                              out=None, softmax_scale=None, max_prefix_len=None, kv_split_tokens=0):
+    """Standard single-block step (paper, Sec. "Block diffusion"): q holds
+    block_size rows per sequence."""
+    lib = load()
+    kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
+    batch = prefix_lens.shape[0]
+    if max_prefix_len is None:
+        max_prefix_len = int(prefix_lens.max().item()) if batch else 0
+    stream = _stream(q.device)
+    opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
+                    int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), None, 0, stream)
+    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+    if need == ctypes.c_size_t(-1).value:
+        need = 0
+    ws = _workspace("attn", q.device, need, stream)
+    opts.workspace = _ptr(ws)
+    opts.workspace_bytes = need
+    _check("block_diffusion_attention", lib.block_diffusion_attention(
+        _ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens), int(block_size), _ptr(out),
+        ctypes.byref(opts)))
+    return out
+
+
+def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
+    """Edit selection (paper, Eq. (1), token-to-token set).  logits: bf16
+    [rows, row_stride] (the first `vocab` columns are used; default all).
+    Returns (new_tokens int32, conf float32, changed_mask uint8)."""
+    lib = load()
+    dev = logits.device
+    _need(cur_tokens, "cur_tokens", torch.int32, dev, 1)
+    if logits.dtype != torch.bfloat16 or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a bf16 [rows, row_stride] tensor with unit column stride")
+    rows = logits.shape[0]
+    if cur_tokens.shape[0] != rows:
+        raise ValueError("cur_tokens must have one entry per row")
+    v = logits.shape[1] if vocab is None else int(vocab)
+    ld = logits.stride(0) if rows > 1 else max(logits.shape[1], 1)
+    if out is None:
+        new = torch.empty(rows, dtype=torch.int32, device=dev)
+        conf = torch.empty(rows, dtype=torch.float32, device=dev)
+        changed = torch.empty(rows, dtype=torch.uint8, device=dev)
+    else:
+        new, conf, changed = out
+    stream = _stream(dev)
+    need = lib.mbe_edit_select_workspace_size(rows, v)
+    ws = _workspace("edit", dev, need if need != ctypes.c_size_t(-1).value else 0, stream)
+    _check("mbe_edit_select", lib.mbe_edit_select(
+        _ptr(logits), rows, v, ld, _ptr(cur_tokens), ctypes.c_float(threshold), _ptr(new), _ptr(conf),
+        _ptr(changed), _ptr(ws), need if ws is not None else 0, stream))
+    return new, conf, changed

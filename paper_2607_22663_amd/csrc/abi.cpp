@@ -1,0 +1,332 @@
+// C ABI of libmbe: argument validation, split planning, workspace sizing and
+// dispatch to the HIP kernels.  Every check runs before the first HIP call,
+// so the validation paths work on a machine without a GPU.
+#include "../../include/mbe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mbe_status fail(mbe_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+mbe_status hip_fail(hipError_t e, const char *where) {
+  return fail(MBE_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool debug_checks() {
+  const char *v = std::getenv("MBE_DEBUG_CHECK");
+  return v && v[0] == '1';
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Split-KV plan for the attention calls, from host-known bounds only.
+struct AttnPlan {
+  int32_t group = 0, qtiles = 0, splits = 1, kv_chunk = 0;
+  int64_t units = 0, units_per_xcd = 0;
+  size_t counters_off = 0, part_o_off = 0, part_ml_off = 0, bytes = 0;
+};
+
+mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_t block_size,
+                          int32_t window_bound, AttnPlan *pl) {
+  if (!kv) return fail(MBE_ERR_NULL_ARG, "paged_kv is NULL");
+  if (!o) return fail(MBE_ERR_NULL_ARG, "opts is NULL");
+  if (kv->page_size != mbe::kPageSize)
+    return fail(MBE_ERR_UNSUPPORTED, "page_size %d: only 16-token pages are supported", kv->page_size);
+  if (kv->head_dim != 64 && kv->head_dim != 128)
+    return fail(MBE_ERR_UNSUPPORTED, "head_dim %d: supported are 64 and 128", kv->head_dim);
+  if (kv->num_kv_heads < 1) return fail(MBE_ERR_BAD_SHAPE, "num_kv_heads %d < 1", kv->num_kv_heads);
+  if (kv->num_pages < 0) return fail(MBE_ERR_BAD_SHAPE, "num_pages %d < 0", kv->num_pages);
+  if (o->batch < 0) return fail(MBE_ERR_BAD_SHAPE, "batch %d < 0", o->batch);
+  if (o->num_q_heads < 1 || o->num_q_heads % kv->num_kv_heads != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "num_q_heads %d is not a positive multiple of num_kv_heads %d",
+                o->num_q_heads, kv->num_kv_heads);
+  if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
+  if (o->total_q < 0 || o->max_prefix_len < 0 || window_bound < 0 || o->max_pages_per_seq < 0)
+    return fail(MBE_ERR_BAD_SHAPE, "negative total_q/max_prefix_len/max_window_len/max_pages_per_seq");
+  if (window_bound % block_size != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "max_window_len %d is not a multiple of block_size %d", window_bound,
+                block_size);
+  if (o->mask_mode != MBE_MASK_WINDOW_BIDIR && o->mask_mode != MBE_MASK_BLOCK_CAUSAL)
+    return fail(MBE_ERR_UNSUPPORTED, "mask_mode %d", o->mask_mode);
+  if (o->softmax_scale != o->softmax_scale) return fail(MBE_ERR_BAD_VALUE, "softmax_scale is NaN");
+  if (o->kv_split_tokens < 0 || o->kv_split_tokens % mbe::kKeyTile != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "kv_split_tokens %d is not 0 or a positive multiple of 64",
+                o->kv_split_tokens);
+  const int64_t max_kv = static_cast<int64_t>(o->max_prefix_len) + window_bound;
+  if (o->batch > 0 && max_kv > 0 && o->max_pages_per_seq < 1)
+    return fail(MBE_ERR_BAD_SHAPE, "max_pages_per_seq must be >= 1");
+  if (max_kv > (1LL << 30)) return fail(MBE_ERR_BAD_SHAPE, "sequence bound too large");
+  if (o->batch > 0 && kv->num_pages < 1 && max_kv > 0) return fail(MBE_ERR_BAD_SHAPE, "empty page pool");
+
+  pl->group = o->num_q_heads / kv->num_kv_heads;
+  const int64_t rows = static_cast<int64_t>(pl->group) * window_bound;
+  pl->qtiles = static_cast<int32_t>(std::max<int64_t>(1, (rows + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile));
+  const int64_t base_units = static_cast<int64_t>(o->batch) * kv->num_kv_heads * pl->qtiles;
+
+  int64_t chunk = o->kv_split_tokens;
+  if (chunk == 0 && base_units > mbe::kMaxCounters) {
+    chunk = std::max<int64_t>(max_kv, 1);   // enough work units without splitting
+  } else if (chunk == 0) {
+    // Aim for about 4 workgroups per CU over 256 CUs, but keep splits at
+    // least 1024 keys long so that partial results stay a small fraction of
+    // the K/V traffic.
+    const int64_t target_units = 1024;
+    int64_t splits = base_units > 0 ? (target_units + base_units - 1) / base_units : 1;
+    const int64_t max_splits = std::max<int64_t>(1, max_kv / 1024);
+    splits = std::min(std::max<int64_t>(splits, 1), max_splits);
+    chunk = (max_kv + splits - 1) / splits;
+  }
+  chunk = std::max<int64_t>(mbe::kKeyTile, (chunk + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
+  pl->kv_chunk = static_cast<int32_t>(chunk);
+  pl->splits = static_cast<int32_t>(std::max<int64_t>(1, (max_kv + chunk - 1) / chunk));
+  pl->units = base_units * pl->splits;
+  pl->units_per_xcd = (pl->units + mbe::kXcds - 1) / mbe::kXcds;
+  if (pl->units_per_xcd * mbe::kXcds > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "grid too large");
+
+  pl->bytes = 0;
+  if (pl->splits > 1) {
+    if (base_units > mbe::kMaxCounters)
+      return fail(MBE_ERR_UNSUPPORTED, "split-KV over %lld query tiles exceeds %lld; use kv_split_tokens = 0",
+                  static_cast<long long>(base_units), static_cast<long long>(mbe::kMaxCounters));
+    const size_t rows_all = static_cast<size_t>(pl->splits) * o->total_q * o->num_q_heads;
+    pl->counters_off = 0;
+    pl->part_o_off = mbe::kCounterBytes;
+    pl->part_ml_off = pl->part_o_off + align_up(rows_all * kv->head_dim * sizeof(float));
+    pl->bytes = pl->part_ml_off + align_up(rows_all * 2 * sizeof(float));
+  }
+  return MBE_OK;
+}
+
+mbe_status debug_check_attention(const mbe_paged_kv *kv, const int32_t *page_table, const int32_t *prefix_lens,
+                                 const int32_t *window_lens, int32_t block_size, int32_t fixed_window,
+                                 const mbe_attn_opts *o) {
+  const int B = o->batch;
+  std::vector<int32_t> P(B), W(B, fixed_window), T(static_cast<size_t>(B) * o->max_pages_per_seq);
+  hipError_t e = hipMemcpy(P.data(), prefix_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && fixed_window < 0)
+    e = hipMemcpy(W.data(), window_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && !T.empty())
+    e = hipMemcpy(T.data(), page_table, T.size() * sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "MBE_DEBUG_CHECK copy");
+  int64_t tq = 0;
+  for (int b = 0; b < B; ++b) {
+    if (P[b] < 0 || P[b] > o->max_prefix_len)
+      return fail(MBE_ERR_BAD_VALUE, "prefix_lens[%d] = %d outside [0, %d]", b, P[b], o->max_prefix_len);
+    const int wb = fixed_window >= 0 ? fixed_window : o->max_window_len;
+    if (W[b] < 0 || W[b] > wb || W[b] % block_size != 0)
+      return fail(MBE_ERR_BAD_VALUE, "window_lens[%d] = %d invalid", b, W[b]);
+    tq += W[b];
+    const int np = (P[b] + W[b] + mbe::kPageSize - 1) / mbe::kPageSize;
+    if (np > o->max_pages_per_seq)
+      return fail(MBE_ERR_BAD_VALUE, "sequence %d needs %d pages > max_pages_per_seq %d", b, np,
+                  o->max_pages_per_seq);
+    for (int j = 0; j < np; ++j) {
+      const int32_t pg = T[static_cast<size_t>(b) * o->max_pages_per_seq + j];
+      if (pg < 0 || pg >= kv->num_pages)
+        return fail(MBE_ERR_BAD_VALUE, "page_table[%d][%d] = %d outside [0, %d)", b, j, pg, kv->num_pages);
+    }
+  }
+  if (tq != o->total_q)
+    return fail(MBE_ERR_BAD_VALUE, "sum of window lengths %lld != total_q %d", static_cast<long long>(tq),
+                o->total_q);
+  return MBE_OK;
+}
+
+mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *page_table,
+                         const int32_t *prefix_lens, const int32_t *window_lens, int32_t block_size,
+                         int32_t fixed_window, void *out, const mbe_attn_opts *o) {
+  const int32_t window_bound = fixed_window >= 0 ? fixed_window : (o ? o->max_window_len : 0);
+  AttnPlan pl;
+  mbe_status st = plan_attention(kv, o, block_size, window_bound, &pl);
+  if (st != MBE_OK) return st;
+  if (fixed_window >= 0 && o->total_q != static_cast<int64_t>(o->batch) * fixed_window)
+    return fail(MBE_ERR_BAD_SHAPE, "total_q %d != batch %d * block_size %d", o->total_q, o->batch,
+                fixed_window);
+  if (o->batch == 0 || o->total_q == 0) return MBE_OK;
+  if (!q || !out || !page_table || !prefix_lens || !kv->k_pages || !kv->v_pages)
+    return fail(MBE_ERR_NULL_ARG, "q, out, page_table, prefix_lens, k_pages and v_pages must be non-NULL");
+  if (fixed_window < 0 && !window_lens) return fail(MBE_ERR_NULL_ARG, "window_lens is NULL");
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(out) |
+       reinterpret_cast<uintptr_t>(kv->k_pages) | reinterpret_cast<uintptr_t>(kv->v_pages)) % 16 != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "q, out, k_pages and v_pages must be 16-byte aligned");
+  if (pl.bytes > 0) {
+    if (!o->workspace) return fail(MBE_ERR_WORKSPACE, "workspace of %zu bytes required", pl.bytes);
+    if (o->workspace_bytes < pl.bytes)
+      return fail(MBE_ERR_WORKSPACE, "workspace %zu bytes < required %zu", o->workspace_bytes, pl.bytes);
+    if (reinterpret_cast<uintptr_t>(o->workspace) % 256 != 0)
+      return fail(MBE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  if (debug_checks()) {
+    st = debug_check_attention(kv, page_table, prefix_lens, window_lens, block_size, fixed_window, o);
+    if (st != MBE_OK) return st;
+  }
+
+  mbe::AttnParams p{};
+  p.q = static_cast<const uint16_t *>(q);
+  p.k_pages = static_cast<const uint16_t *>(kv->k_pages);
+  p.v_pages = static_cast<const uint16_t *>(kv->v_pages);
+  p.page_table = page_table;
+  p.prefix_lens = prefix_lens;
+  p.window_lens = window_lens;
+  p.out = static_cast<uint16_t *>(out);
+  char *ws = static_cast<char *>(o->workspace);
+  p.counters = pl.bytes ? reinterpret_cast<uint32_t *>(ws + pl.counters_off) : nullptr;
+  p.part_o = pl.bytes ? reinterpret_cast<float *>(ws + pl.part_o_off) : nullptr;
+  p.part_ml = pl.bytes ? reinterpret_cast<float *>(ws + pl.part_ml_off) : nullptr;
+  p.batch = o->batch;
+  p.num_q_heads = o->num_q_heads;
+  p.num_kv_heads = kv->num_kv_heads;
+  p.group = pl.group;
+  p.num_pages = kv->num_pages;
+  p.max_pages = o->max_pages_per_seq;
+  p.block_size = block_size;
+  p.total_q = o->total_q;
+  p.fixed_window = fixed_window;
+  p.max_prefix = o->max_prefix_len;
+  p.max_window = window_bound;
+  p.qtiles = pl.qtiles;
+  p.splits = pl.splits;
+  p.kv_chunk = pl.kv_chunk;
+  p.units = pl.units;
+  p.units_per_xcd = pl.units_per_xcd;
+  const float scale = o->softmax_scale > 0.f ? o->softmax_scale : 1.0f / std::sqrt(static_cast<float>(kv->head_dim));
+  p.scale_log2 = scale * 1.4426950408889634f;
+  const int mode = fixed_window >= 0 ? MBE_MASK_WINDOW_BIDIR : o->mask_mode;
+  hipError_t e = mbe::launch_window_attention(p, kv->head_dim, mode, static_cast<hipStream_t>(o->stream));
+  if (e != hipSuccess) return hip_fail(e, "window attention launch");
+  return MBE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mbe_status mbe_window_attention(const void *q, const mbe_paged_kv *paged_kv, const int32_t *page_table,
+                                const int32_t *prefix_lens, const int32_t *window_lens, int32_t block_size,
+                                void *out, const mbe_attn_opts *opts) {
+  return run_attention(q, paged_kv, page_table, prefix_lens, window_lens, block_size, -1, out, opts);
+}
+
+mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv, const int32_t *page_table,
+                                     const int32_t *prefix_lens, int32_t block_size, void *out,
+                                     const mbe_attn_opts *opts) {
+  if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
+  return run_attention(q, paged_kv, page_table, prefix_lens, nullptr, block_size, block_size, out, opts);
+}
+
+size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts,
+                                           int32_t block_size) {
+  AttnPlan pl;
+  if (!opts) return static_cast<size_t>(-1);
+  if (plan_attention(paged_kv, opts, block_size, opts->max_window_len, &pl) != MBE_OK)
+    return static_cast<size_t>(-1);
+  return pl.bytes;
+}
+
+size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab) {
+  if (rows < 0 || vocab < 0) return static_cast<size_t>(-1);
+  if (rows == 0 || vocab == 0) return 0;
+  int32_t chunks;
+  int64_t len;
+  mbe::edit_select_plan(rows, vocab, &chunks, &len);
+  if (chunks <= 1) return 0;
+  return mbe::kCounterBytes + align_up(static_cast<size_t>(rows) * chunks * sizeof(mbe::EsPartial));
+}
+
+mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                           const int32_t *cur_tokens, float threshold, int32_t *new_tokens, float *conf,
+                           uint8_t *changed_mask, void *workspace, size_t workspace_bytes, void *stream) {
+  if (rows < 0 || vocab < 0) return fail(MBE_ERR_BAD_SHAPE, "rows %lld / vocab %lld negative",
+                                         static_cast<long long>(rows), static_cast<long long>(vocab));
+  if (rows > 0 && vocab < 1) return fail(MBE_ERR_BAD_SHAPE, "vocab must be >= 1");
+  if (row_stride < vocab)
+    return fail(MBE_ERR_BAD_SHAPE, "row_stride %lld < vocab %lld", static_cast<long long>(row_stride),
+                static_cast<long long>(vocab));
+  if (vocab > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "vocab beyond int32 indices");
+  if (threshold != threshold) return fail(MBE_ERR_BAD_VALUE, "threshold is NaN");
+  if (rows == 0) return MBE_OK;
+  if (!logits || !cur_tokens || !new_tokens || !conf || !changed_mask)
+    return fail(MBE_ERR_NULL_ARG, "logits, cur_tokens, new_tokens, conf and changed_mask must be non-NULL");
+  int32_t chunks;
+  int64_t len;
+  mbe::edit_select_plan(rows, vocab, &chunks, &len);
+  if (rows * chunks > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "too many rows");
+  const size_t need = mbe_edit_select_workspace_size(rows, vocab);
+  if (need > 0) {
+    if (!workspace) return fail(MBE_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+    if (workspace_bytes < need)
+      return fail(MBE_ERR_WORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+    if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+      return fail(MBE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  mbe::EsParams p{};
+  p.logits = static_cast<const uint16_t *>(logits);
+  p.rows = rows;
+  p.vocab = vocab;
+  p.ld = row_stride;
+  p.chunk_len = len;
+  p.chunks = chunks;
+  p.cur = cur_tokens;
+  p.threshold = threshold;
+  p.new_tokens = new_tokens;
+  p.conf = conf;
+  p.changed = changed_mask;
+  if (need > 0) {
+    char *ws = static_cast<char *>(workspace);
+    p.counters = reinterpret_cast<uint32_t *>(ws);
+    p.partials = reinterpret_cast<mbe::EsPartial *>(ws + mbe::kCounterBytes);
+  }
+  const bool vec = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && (row_stride % 8 == 0);
+  hipError_t e = mbe::launch_edit_select(p, vec, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "edit select launch");
+  return MBE_OK;
+}
+
+mbe_status mbe_workspace_zero(void *workspace, size_t bytes, void *stream) {
+  if (bytes == 0) return MBE_OK;
+  if (!workspace) return fail(MBE_ERR_NULL_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+    return fail(MBE_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  hipError_t e = mbe::launch_zero_fill(workspace, bytes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "workspace zero fill");
+  return MBE_OK;
+}
+
+const char *mbe_status_string(mbe_status s) {
+  switch (s) {
+    case MBE_OK: return "ok";
+    case MBE_ERR_NULL_ARG: return "null argument";
+    case MBE_ERR_BAD_SHAPE: return "bad shape";
+    case MBE_ERR_UNSUPPORTED: return "unsupported";
+    case MBE_ERR_WORKSPACE: return "workspace missing or too small";
+    case MBE_ERR_HIP: return "HIP error";
+    case MBE_ERR_BAD_VALUE: return "bad value";
+  }
+  return "unknown status";
+}
+
+const char *mbe_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

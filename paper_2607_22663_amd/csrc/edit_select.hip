@@ -1,0 +1,241 @@
+// Confidence-based edit selection over vocabulary logits, gfx950.
+//
+// Paper, Sec. "Configurable threshold decoding", Eq. (1): per position, the
+// prediction is the highest-probability token and its confidence is that
+// probability; a visible token is overwritten (the token-to-token set) when
+// the prediction differs from it and the confidence clears the threshold.
+// MBE keeps this rule for its cross-block passes (Sec. "Training-Free MBE
+// Decoding").  Ties go to the lowest index; the test is conf >= threshold.
+//
+// One HBM pass per row.  Each workgroup (256 threads) reduces one chunk of a
+// row; each thread streams 16-byte bf16 vectors, 4 in flight, and keeps
+//   m       its running maximum,
+//   s       sum of exp(x - m), rescaled when m grows,
+//   it_max  the iteration where m was first reached.
+// Elements of one thread are visited in increasing index order, so its first
+// occurrence of m lies in iteration it_max; that iteration is re-read once at
+// the end to find the index (64 bytes per thread, from cache), which keeps
+// the argmax bookkeeping out of the per-element loop.
+// Threads then merge (max, lowest index among equals, rescaled sum) in a
+// fixed tree; rows split over several workgroups write partials, and the
+// last workgroup of the row (atomic arrival counter, reset after use) merges
+// them in chunk order, so results are bitwise reproducible.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace mbe {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kU = kEsVecPerThread;
+constexpr int kT = kEsThreads;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_at(const uint16_t *p) {
+  return __uint_as_float(static_cast<uint32_t>(*p) << 16);
+}
+
+// exp(d) for d <= 0 through the hardware base-2 exponential.
+__device__ __forceinline__ float exp_neg(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
+
+// Merge partial (m, s, i) with (m2, s2, i2): larger max wins, equal maxima keep
+// the lower index, sums are rescaled to the common max.
+__device__ __forceinline__ void merge(float &m, float &s, int32_t &i, float m2, float s2, int32_t i2) {
+  const float M = fmaxf(m, m2);
+  if (M == -INFINITY) {       // both empty so far
+    i = min(i, i2);
+    return;
+  }
+  const float a = (m == -INFINITY) ? 0.f : s * exp_neg(m - M);
+  const float b = (m2 == -INFINITY) ? 0.f : s2 * exp_neg(m2 - M);
+  s = a + b;
+  i = (m > m2) ? i : ((m2 > m) ? i2 : min(i, i2));
+  m = M;
+}
+
+// Loads vector unit `unit` (elements 8*unit .. 8*unit+7) as 8 floats; elements
+// at or beyond `end` read as -inf.
+template <bool VEC>
+__device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int64_t end, float x[8]) {
+  const int64_t e0 = unit * 8;
+  if (VEC && e0 + 8 <= end) {
+    const uint4 w = *reinterpret_cast<const uint4 *>(row + e0);
+    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x);
+    x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
+    x[4] = bf16_lo(w.z); x[5] = bf16_hi(w.z);
+    x[6] = bf16_lo(w.w); x[7] = bf16_hi(w.w);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = (e0 + k < end) ? bf16_at(row + e0 + k) : -INFINITY;
+  }
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
+  __shared__ float sh_m[kT / 64];
+  __shared__ float sh_s[kT / 64];
+  __shared__ int32_t sh_i[kT / 64];
+
+  const int64_t wg = blockIdx.x;
+  const int64_t row = wg / p.chunks;
+  const int32_t chunk = static_cast<int32_t>(wg % p.chunks);
+  const int tid = threadIdx.x;
+  const uint16_t *rowp = p.logits + row * p.ld;
+  const int64_t c0 = static_cast<int64_t>(chunk) * p.chunk_len;
+  const int64_t c1 = min(p.vocab, c0 + p.chunk_len);
+  const int64_t u0 = c0 / 8;
+  const int64_t u1 = (c1 + 7) / 8;
+
+  float m = -INFINITY, s = 0.f;
+  int32_t it_max = -1;
+  int32_t it = 0;
+  for (int64_t base = u0; base < u1; base += kT * kU, ++it) {
+    float x[kU][8];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t unit = base + j * kT + tid;
+      if (unit < u1) {
+        load_unit<VEC>(rowp, unit, c1, x[j]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[j][k] = -INFINITY;
+      }
+    }
+    float cm = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kU; ++j)
+#pragma unroll
+      for (int k = 0; k < 8; k += 2) cm = fmaxf(cm, fmaxf(x[j][k], x[j][k + 1]));
+    if (cm > m) {
+      s = (m == -INFINITY) ? 0.f : s * exp_neg(m - cm);
+      m = cm;
+      it_max = it;
+    }
+    const float ms = (m == -INFINITY) ? 0.f : m;
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < kU; ++j)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc += exp_neg(x[j][k] - ms);
+    s += acc;
+  }
+
+  // First index of m among this thread's elements: it lies in iteration it_max.
+  int32_t idx = INT32_MAX;
+  if (it_max >= 0) {
+    const int64_t base = u0 + static_cast<int64_t>(it_max) * kT * kU;
+    for (int j = 0; j < kU && idx == INT32_MAX; ++j) {
+      const int64_t unit = base + j * kT + tid;
+      if (unit >= u1) break;
+      float x[8];
+      load_unit<VEC>(rowp, unit, c1, x);
+      for (int k = 0; k < 8; ++k) {
+        if (x[k] == m) {
+          idx = static_cast<int32_t>(unit * 8 + k);
+          break;
+        }
+      }
+    }
+  }
+
+  // Wave reduction in a fixed butterfly order.
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o);
+    const float s2 = __shfl_xor(s, o);
+    const int32_t i2 = __shfl_xor(idx, o);
+    merge(m, s, idx, m2, s2, i2);
+  }
+  const int wave = tid / 64;
+  if ((tid & 63) == 0) {
+    sh_m[wave] = m;
+    sh_s[wave] = s;
+    sh_i[wave] = idx;
+  }
+  __syncthreads();
+  if (tid != 0) return;
+  m = sh_m[0];
+  s = sh_s[0];
+  idx = sh_i[0];
+  for (int w = 1; w < kT / 64; ++w) merge(m, s, idx, sh_m[w], sh_s[w], sh_i[w]);
+
+  if (p.chunks > 1) {
+    p.partials[row * p.chunks + chunk] = EsPartial{m, s, idx, 0};
+    __threadfence();
+    const uint32_t arrived = atomicAdd(&p.counters[row], 1u);
+    if (arrived != static_cast<uint32_t>(p.chunks - 1)) return;
+    __threadfence();
+    const EsPartial *pp = p.partials + row * p.chunks;
+    EsPartial first = pp[0];
+    m = first.m;
+    s = first.s;
+    idx = first.idx;
+    for (int c = 1; c < p.chunks; ++c) {
+      const EsPartial q = pp[c];
+      merge(m, s, idx, q.m, q.s, q.idx);
+    }
+    p.counters[row] = 0u;     // ready for the next call
+  }
+
+  const int32_t cur = p.cur[row];
+  const float conf = 1.0f / s;          // correctly rounded division
+  const bool change = (m != -INFINITY) && (idx != cur) && (conf >= p.threshold);
+  p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
+  p.new_tokens[row] = change ? idx : cur;
+  p.changed[row] = change ? 1 : 0;
+}
+
+__global__ void zero_fill_kernel(uint4 *p, size_t n16, uint8_t *tail, size_t ntail) {
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride)
+    p[i] = make_uint4(0, 0, 0, 0);
+  if (blockIdx.x == 0)
+    for (size_t i = threadIdx.x; i < ntail; i += blockDim.x) tail[i] = 0;
+}
+
+}  // namespace
+
+void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len) {
+  // Enough workgroups to cover 256 CUs several times over; a chunk keeps at
+  // least 4096 elements so each thread still streams two full iterations.
+  const int64_t target_wgs = 2048;
+  int64_t c = 1;
+  if (rows < target_wgs && rows <= kMaxCounters) {
+    c = (target_wgs + rows - 1) / rows;
+    const int64_t max_c = (vocab + 4095) / 4096;
+    if (c > max_c) c = max_c;
+    if (c > 1024) c = 1024;
+    if (c < 1) c = 1;
+  }
+  int64_t len = (vocab + c - 1) / c;
+  len = (len + 7) / 8 * 8;
+  c = (vocab + len - 1) / len;
+  if (c < 1) c = 1;
+  *chunks = static_cast<int32_t>(c);
+  *chunk_len = len;
+}
+
+hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>(p.rows * p.chunks));
+  if (vector_loads)
+    hipLaunchKernelGGL(edit_select_kernel<true>, grid, dim3(kT), 0, stream, p);
+  else
+    hipLaunchKernelGGL(edit_select_kernel<false>, grid, dim3(kT), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_fill(void *ptr, size_t bytes, hipStream_t stream) {
+  const size_t n16 = bytes / 16;
+  const size_t ntail = bytes - n16 * 16;
+  size_t blocks = (n16 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(zero_fill_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
+                     reinterpret_cast<uint4 *>(ptr), n16, static_cast<uint8_t *>(ptr) + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+}  // namespace mbe

@@ -1,0 +1,78 @@
+// Internal launch interface between the C ABI (abi.cpp) and the HIP kernels.
+// Not installed; callers use include/mbe.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mbe {
+
+// ---------------------------------------------------------------- attention
+constexpr int kPageSize = 16;
+constexpr int kKeyTile = 64;          // keys per LDS tile (4 pages)
+constexpr int kRowsPerWave = 64;      // packed (window position, q head) rows per wave
+constexpr int kWaves = 4;
+constexpr int kRowsPerTile = kRowsPerWave * kWaves;   // rows per workgroup
+constexpr int kXcds = 8;              // MI355X: workgroups go round-robin over 8 XCDs
+
+// Every workspace starts with a fixed region of arrival counters.  It is
+// zero-filled once and every call leaves the counters it used at zero; no
+// call ever writes partial results into it, whatever the shapes, so a
+// workspace can be reused across calls of different shapes.
+constexpr size_t kCounterBytes = 65536;
+constexpr int64_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
+
+struct AttnParams {
+  const uint16_t *q;          // bf16 [total_q][Hq][D]
+  const uint16_t *k_pages;    // bf16 [num_pages][Hkv][16][D]
+  const uint16_t *v_pages;    // bf16 [num_pages][Hkv][D][16]
+  const int32_t *page_table;  // [batch][max_pages]
+  const int32_t *prefix_lens; // [batch]
+  const int32_t *window_lens; // [batch] (unused when fixed_window >= 0)
+  uint16_t *out;              // bf16 [total_q][Hq][D]
+  float *part_o;              // fp32 [splits][total_q][Hq][D]   (split-KV only)
+  float *part_ml;             // fp32 [splits][total_q][Hq][2]   (split-KV only)
+  uint32_t *counters;         // [batch][Hkv][qtiles]            (split-KV only)
+  int32_t batch, num_q_heads, num_kv_heads, group, num_pages, max_pages;
+  int32_t block_size, total_q, fixed_window;
+  int32_t max_prefix, max_window;   // host-validated bounds; device lengths are clamped to them
+  int32_t qtiles, splits, kv_chunk;
+  int64_t units, units_per_xcd;
+  float scale_log2;           // softmax scale * log2(e)
+};
+
+hipError_t launch_window_attention(const AttnParams &p, int head_dim, int mask_mode,
+                                   hipStream_t stream);
+
+// ------------------------------------------------------------ edit selection
+constexpr int kEsThreads = 256;
+constexpr int kEsVecPerThread = 4;   // 16-byte loads per thread per iteration
+
+struct EsPartial {
+  float m;        // running max logit
+  float s;        // sum of exp(l - m)
+  int32_t idx;    // lowest index attaining m
+  int32_t pad;
+};
+
+struct EsParams {
+  const uint16_t *logits;   // bf16 [rows][ld]
+  int64_t rows, vocab, ld;
+  int64_t chunk_len;        // elements per chunk, a multiple of 8
+  int32_t chunks;           // chunks per row
+  const int32_t *cur;
+  float threshold;
+  int32_t *new_tokens;
+  float *conf;
+  uint8_t *changed;
+  EsPartial *partials;      // [rows][chunks]   (chunks > 1 only)
+  uint32_t *counters;       // [rows]           (chunks > 1 only)
+};
+
+void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len);
+hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream);
+
+hipError_t launch_zero_fill(void *ptr, size_t bytes, hipStream_t stream);
+
+}  // namespace mbe

@@ -1,0 +1,148 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared
+symbol, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2607_22663_amd as mbe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mbe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(mbe_\w+|block_diffusion_attention)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mbe.LIB_PATH):
+        pytest.fail("libmbe.so is not built (run python -m paper_2607_22663_amd.build)")
+    return mbe.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert len(names) == 8, names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(mbe.EXPORTS)
+
+
+def _kv(head_dim=128, page=16, hkv=4, pages=10):
+    return mbe.PagedKV(ctypes.c_void_p(16), ctypes.c_void_p(32), pages, page, hkv, head_dim)
+
+
+def _opts(**kw):
+    base = dict(batch=1, num_q_heads=16, max_pages_per_seq=10, total_q=64, max_prefix_len=64,
+                max_window_len=64, mask_mode=0, softmax_scale=0.0, kv_split_tokens=0,
+                workspace=None, workspace_bytes=0, stream=None)
+    base.update(kw)
+    return mbe.AttnOpts(**base)
+
+
+def _attn(lib, kv, opts, B=32, q=16, out=48):
+    st = lib.mbe_window_attention(ctypes.c_void_p(q), ctypes.byref(kv), ctypes.c_void_p(8),
+                                  ctypes.c_void_p(8), ctypes.c_void_p(8), B, ctypes.c_void_p(out),
+                                  ctypes.byref(opts))
+    return st, lib.mbe_last_error().decode()
+
+
+@pytest.mark.parametrize("kv_kw,opt_kw,B,status,text", [
+    (dict(head_dim=96), {}, 32, 3, "head_dim"),
+    (dict(page=32), {}, 32, 3, "page_size"),
+    ({}, dict(num_q_heads=6), 32, 2, "multiple"),
+    ({}, dict(max_window_len=48), 32, 2, "multiple of block_size"),
+    ({}, dict(max_pages_per_seq=0), 32, 2, "max_pages_per_seq"),
+    ({}, dict(mask_mode=5), 32, 3, "mask_mode"),
+    ({}, dict(kv_split_tokens=100), 32, 2, "multiple of 64"),
+    ({}, dict(softmax_scale=float("nan")), 32, 6, "NaN"),
+    ({}, dict(batch=-1), 32, 2, "batch"),
+    ({}, {}, 0, 2, "block_size"),
+])
+def test_attention_validation(lib, kv_kw, opt_kw, B, status, text):
+    st, msg = _attn(lib, _kv(**kv_kw), _opts(**opt_kw), B=B)
+    assert st == status and text in msg, (st, msg)
+
+
+def test_attention_null_pointers_and_workspace(lib):
+    kv = _kv()
+    st = lib.mbe_window_attention(None, ctypes.byref(kv), None, None, None, 32, None,
+                                  ctypes.byref(_opts()))
+    assert st == 1
+    st = lib.mbe_window_attention(None, None, None, None, None, 32, None, ctypes.byref(_opts()))
+    assert st == 1 and "paged_kv" in lib.mbe_last_error().decode()
+    # a plan that needs split-KV partials without a workspace
+    opts = _opts(max_prefix_len=4096, max_pages_per_seq=300, kv_split_tokens=1024)
+    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32)
+    assert need > 0
+    st, msg = _attn(lib, kv, opts)
+    assert st == 4 and "workspace" in msg
+    opts.workspace, opts.workspace_bytes = ctypes.c_void_p(256), need - 1
+    st, msg = _attn(lib, kv, opts)
+    assert st == 4
+
+
+def test_attention_empty_batch_is_ok_without_launch(lib):
+    st, _ = _attn(lib, _kv(), _opts(batch=0, total_q=0))
+    assert st == 0
+    st, _ = _attn(lib, _kv(), _opts(total_q=0))
+    assert st == 0
+
+
+def test_workspace_sizes(lib):
+    kv = _kv()
+    small = _opts(max_prefix_len=64, kv_split_tokens=0)
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(small), 32) == 0
+    big = _opts(batch=1, total_q=64, max_prefix_len=16384, max_pages_per_seq=1100, kv_split_tokens=2048)
+    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(big), 32)
+    splits = math.ceil((16384 + 64) / 2048)
+    assert n >= splits * 64 * 16 * (128 + 2) * 4
+    bad = _opts(num_q_heads=5)
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(bad), 32) == ctypes.c_size_t(-1).value
+    assert lib.mbe_edit_select_workspace_size(8192, 131072) == 0
+    assert lib.mbe_edit_select_workspace_size(64, 131072) > 0
+    assert lib.mbe_edit_select_workspace_size(-1, 10) == ctypes.c_size_t(-1).value
+
+
+@pytest.mark.parametrize("args,status,text", [
+    (dict(rows=-1), 2, "negative"),
+    (dict(row_stride=100, vocab=128), 2, "row_stride"),
+    (dict(threshold=float("nan")), 6, "NaN"),
+    (dict(logits=None), 1, "non-NULL"),
+    (dict(rows=64, vocab=131072, row_stride=131072, ws=None), 4, "workspace"),
+])
+def test_edit_select_validation(lib, args, status, text):
+    a = dict(logits=16, rows=4, vocab=128, row_stride=128, cur=8, threshold=0.9, new=8, conf=8, ch=8,
+             ws=None, wsb=0)
+    a.update(args)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    st = lib.mbe_edit_select(vp(a["logits"]), a["rows"], a["vocab"], a["row_stride"], vp(a["cur"]),
+                             ctypes.c_float(a["threshold"]), vp(a["new"]), vp(a["conf"]), vp(a["ch"]),
+                             vp(a["ws"]), a["wsb"], None)
+    assert st == status and text in lib.mbe_last_error().decode()
+
+
+def test_edit_select_zero_rows_ok(lib):
+    assert lib.mbe_edit_select(None, 0, 128, 128, None, ctypes.c_float(0.5), None, None, None, None, 0,
+                               None) == 0
+
+
+def test_status_strings(lib):
+    assert lib.mbe_status_string(0) == b"ok"
+    assert lib.mbe_status_string(5) == b"HIP error"
+    assert lib.mbe_status_string(99) == b"unknown status"
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    import importlib
+    m = importlib.reload(mbe)
+    try:
+        with pytest.raises(RuntimeError, match="not found"):
+            m.load(str(tmp_path / "nope.so"))
+    finally:
+        importlib.reload(mbe)

@@ -1,0 +1,172 @@
+"""GPU parity of window attention / block-diffusion attention with the oracle.
+
+Every case calls libmbe through its C ABI (via the ctypes binding) and
+compares with oracle.window_attention (fp64) on the same seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import assert_attn_close, say, seq_slice
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(autouse=True)
+def _name(request):
+    say(f"\n[gpu] {request.node.nodeid}")
+
+
+def run_case(mbe, case, mode="bidir", **kw):
+    c = case.to(DEV)
+    out = mbe.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens,
+                               case.block_size, mask_mode=mode, **kw)
+    torch.cuda.synchronize()
+    return out.cpu()
+
+
+def oracle_case(case, mode="bidir"):
+    m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
+    return oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table,
+                                   case.prefix_lens, case.window_lens, case.block_size, m)
+
+
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+@pytest.mark.parametrize("name", ["tiny_p64_k2_h4_d64", "single_p2048_k2_gqa16x4_d128"])
+def test_workload_full_parity(gpu, name, mode):
+    case = synth.workload_attention(name)
+    say(f"  workload {name} mode {mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
+    out = run_case(gpu, case, mode)
+    err = assert_attn_close(out, oracle_case(case, mode), f"{name} {mode}")
+    say(f"  max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
+
+
+@pytest.mark.parametrize("split", [64, 128, 1024])
+def test_forced_split_kv(gpu, split):
+    case = synth.workload_attention("single_p2048_k2_gqa16x4_d128")
+    say(f"  kv_split_tokens {split}")
+    out = run_case(gpu, case, "bidir", kv_split_tokens=split)
+    assert_attn_close(out, oracle_case(case), f"split {split}")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_ragged_batch_with_poisoned_tails(gpu, D, mode):
+    spec = synth.AttnSpec(4, 32, 1, ("fixed", 0), 8, 2, D)
+    case = synth.make_attention_case(spec, 21, prefix_lens=[0, 37, 1000, 333],
+                                     window_lens=[32, 96, 64, 0], extra_pages=3,
+                                     tail_fill=float("nan"))
+    say(f"  D={D} mode={mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
+    for split in (0, 64, 256):
+        out = run_case(gpu, case, mode, kv_split_tokens=split)
+        assert_attn_close(out, oracle_case(case, mode), f"ragged D={D} {mode} split={split}")
+
+
+@pytest.mark.parametrize("B", [8, 16])
+def test_small_blocks_block_causal(gpu, B):
+    spec = synth.AttnSpec(2, B, 4, ("fixed", 0), 4, 4, 128)
+    case = synth.make_attention_case(spec, 5, prefix_lens=[200, 13])
+    say(f"  block_size {B}")
+    for mode in ("bidir", "block_causal"):
+        out = run_case(gpu, case, mode, kv_split_tokens=128)
+        assert_attn_close(out, oracle_case(case, mode), f"B={B} {mode}")
+
+
+def test_sharp_scores_online_softmax(gpu):
+    """Q scaled by 8: scores spread over tens of units, so the running maximum
+    moves and the lazy rescale path is exercised."""
+    spec = synth.AttnSpec(2, 32, 2, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 77, prefix_lens=[1500, 700], q_scale=8.0)
+    for split in (0, 256):
+        out = run_case(gpu, case, "bidir", kv_split_tokens=split)
+        assert_attn_close(out, oracle_case(case), f"sharp split={split}")
+
+
+def test_block_diffusion_baseline(gpu):
+    spec = synth.AttnSpec(3, 32, 1, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 9, prefix_lens=[640, 0, 96])
+    c = case.to(DEV)
+    out = gpu.block_diffusion_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, 32)
+    torch.cuda.synchronize()
+    ref = oracle.block_diffusion_attention(case.q, case.k_pages, case.v_pages, case.page_table,
+                                           case.prefix_lens, 32)
+    assert_attn_close(out.cpu(), ref, "block_diffusion_attention")
+    # k = 1: window bidirectional == block-causal == baseline, on the GPU path itself
+    w_bi = run_case(gpu, case, "bidir")
+    w_bc = run_case(gpu, case, "block_causal")
+    assert torch.equal(w_bi, out.cpu()) and torch.equal(w_bc, out.cpu())
+
+
+def test_block_causal_equals_stacked_single_blocks_on_gpu(gpu):
+    spec = synth.AttnSpec(1, 32, 3, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 12, prefix_lens=[512])
+    full = run_case(gpu, case, "block_causal")
+    c = case.to(DEV)
+    for j in range(3):
+        qj = c.q[32 * j:32 * (j + 1)].contiguous()
+        one = gpu.block_diffusion_attention(qj, c.k_pages, c.v_pages, c.page_table, c.prefix_lens + 32 * j, 32)
+        torch.cuda.synchronize()
+        a = full[32 * j:32 * (j + 1)].float()
+        assert (a - one.cpu().float()).abs().max() <= 1e-2, f"block {j}"
+
+
+def test_empty_inputs(gpu):
+    spec = synth.AttnSpec(2, 32, 1, ("fixed", 0), 4, 4, 64)
+    case = synth.make_attention_case(spec, 1, prefix_lens=[64, 16], window_lens=[0, 0])
+    c = case.to(DEV)
+    out = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, 32)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 4, 64)
+
+
+def test_workspace_reuse_across_shapes(gpu):
+    """A workspace reused by a call with more query tiles after a call whose
+    partial results were larger: the counters must not have been overwritten."""
+    for k, split in ((4, 0), (8, 0), (2, 1024), (8, 2048), (1, 0)):
+        case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=k,
+                                        prefix_lens=[4096, 1000, 4000, 64, 2048, 3000, 512, 4096])
+        out = run_case(gpu, case, "bidir", kv_split_tokens=split)
+        for b in (1, 7):
+            q, pt, P, W, rows = seq_slice(case, b)
+            ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size)
+            assert_attn_close(out[rows], ref, f"k={k} split={split} seq {b}")
+
+
+def test_deterministic(gpu):
+    case = synth.workload_attention("single_p2048_k2_gqa16x4_d128")
+    a = run_case(gpu, case, "bidir", kv_split_tokens=256)
+    b = run_case(gpu, case, "bidir", kv_split_tokens=256)
+    assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- full sizes, sampled
+def _sampled_parity(gpu, case, seqs, what, **kw):
+    out = run_case(gpu, case, "bidir", **kw)
+    for b in seqs:
+        q, pt, P, W, rows = seq_slice(case, b)
+        ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size)
+        err = assert_attn_close(out[rows], ref, f"{what} seq {b}")
+        say(f"  {what} seq {b} P={int(P[0])}: max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
+
+
+def test_batch32_sampled(gpu):
+    case = synth.workload_attention("batch32_p512to8192_k2")
+    P = case.prefix_lens.numpy()
+    seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 7})
+    _sampled_parity(gpu, case, seqs, "batch32")
+
+
+@pytest.mark.parametrize("k", synth.SPAN_SWEEP_K)
+def test_span_sweep_sampled(gpu, k):
+    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=k)
+    _sampled_parity(gpu, case, [0, 5], f"span k={k}")
+
+
+def test_long_context_sampled(gpu):
+    case = synth.workload_attention("long_context_b64_p4096to32768_k4")
+    P = case.prefix_lens.numpy()
+    seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 31})
+    _sampled_parity(gpu, case, seqs, "long_context")
