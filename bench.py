@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Throughput of the MBE editing-pass hot path on one MI355X.
+
+One step = one pass of the whole path over one batch: editing-window
+attention (paged prefix + bidirectional window) followed by edit selection
+over the vocabulary logits, both through libmbe's C ABI.  Inputs are seeded
+synthetic tensors (synth/) already resident in HBM.
+
+Default workload: 64 sequences, prefixes 32*U{128..1024} (4096..32768),
+window of k = 4 blocks of 32 (128 queries), 16 query / 4 KV heads, head_dim
+128, 16-token pages, edit selection over 8192 rows x 131072 vocabulary.
+
+Prints one JSON line.  `value` is the step's fraction of MI355X speed of
+light, 100 * (attention FLOP / MFMA peak + edit-select bytes / HBM peak) /
+step time, with the attention TFLOP/s and edit-select GB/s alongside.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk x 2.4 GHz; "2.5 PFLOP/s")
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+DEFAULT_WORKLOAD = "long_context_b64_p4096to32768_k4"
+METRIC = "edit-window attention TFLOP/s (bf16) + edit-select GB/s, % of MI355X peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def attention_work(case):
+    """Algorithmic FLOPs and bytes of one window-attention call (bidirectional):
+    4*D per visible (query, key) pair per query head; K/V read once per KV head,
+    Q read and O written once."""
+    P = case.prefix_lens.numpy().astype(np.int64)
+    W = case.window_lens.numpy().astype(np.int64)
+    D, Hq, Hkv = case.head_dim, case.num_q_heads, case.num_kv_heads
+    flops = 4 * D * Hq * int(np.sum(W * (P + W)))
+    kv_bytes = int(np.sum(P + W)) * Hkv * D * 2 * 2
+    qo_bytes = int(W.sum()) * Hq * D * 2 * 2
+    return flops, kv_bytes + qo_bytes
+
+
+def edit_bytes(rows, vocab):
+    """bf16 logits read once; current token read; new token, confidence and
+    changed flag written (4 + 4 + 4 + 1 bytes per row)."""
+    return rows * vocab * 2 + rows * 13
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("attn_window.hip", "edit_select.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_22663_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 --pmc counters, if they were
+    taken on the current kernel sources; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = t.get(kernel, {})
+    if e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_sample, edit_sample):
+    """Times the fp64 oracle (as it stands) on a bounded sample of the same
+    workload on the host cores, scaled to the whole step."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # threadpoolctl missing: numpy elementwise work is single-threaded
+        cores = 1
+    c = attn_case
+    cu = c.cu_q
+    nb = min(attn_sample, c.batch)
+    rows = slice(0, int(cu[nb]))
+    sub_flops = 4 * c.head_dim * c.num_q_heads * int(np.sum(
+        c.window_lens.numpy()[:nb].astype(np.int64) *
+        (c.prefix_lens.numpy()[:nb].astype(np.int64) + c.window_lens.numpy()[:nb])))
+    t0 = time.perf_counter()
+    oracle.window_attention(c.q[rows], c.k_pages, c.v_pages, c.page_table[:nb], c.prefix_lens[:nb],
+                            c.window_lens[:nb], c.block_size)
+    t_attn = time.perf_counter() - t0
+    attn_rate = sub_flops / t_attn                        # flop/s
+    er = min(edit_sample, edit_case.logits.shape[0])
+    t0 = time.perf_counter()
+    oracle.edit_select(edit_case.logits[:er], edit_case.cur_tokens[:er], edit_case.threshold)
+    t_edit = time.perf_counter() - t0
+    edit_rate = edit_bytes(er, edit_case.logits.shape[1]) / t_edit   # byte/s
+    t_step = flops_total / attn_rate + edit_bytes_total / edit_rate
+    sol = flops_total / (PEAK_BF16_TFLOPS * 1e12) + edit_bytes_total / (PEAK_HBM_GBS * 1e9)
+    return {
+        "value": 100.0 * sol / t_step,
+        "unit": "% of MI355X peak (speed-of-light step time / oracle step time)",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"fp64 numpy oracle: window attention of the first {nb} of {c.batch} sequences "
+                   f"({sub_flops / 1e9:.1f} GFLOP, {t_attn:.1f} s) and edit selection of the first {er} "
+                   f"of {edit_case.logits.shape[0]} rows ({edit_bytes(er, edit_case.logits.shape[1]) / 1e6:.0f} MB, "
+                   f"{t_edit:.1f} s), scaled to the full step"),
+        "attention_gflops": attn_rate / 1e9,
+        "edit_select_gbs": edit_rate / 1e9,
+        "step_s": t_step,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--k", type=int, default=None, help="window blocks (span sweep workload)")
+    ap.add_argument("--kv-split-tokens", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--attn-sample", type=int, default=4, help="sequences the CPU oracle times")
+    ap.add_argument("--edit-sample", type=int, default=512, help="edit rows the CPU oracle times")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus} GPUs, WORLD_SIZE={world}); "
+              "this build has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2607_22663_amd as mbe
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    mbe.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    wl = synth.WORKLOADS[args.workload]
+    print(f"[bench] generating {args.workload} (seed {wl.seed})", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    attn_case = synth.workload_attention(args.workload, k_blocks=args.k)
+    edit_case = synth.workload_edit(args.workload) if wl.edit is not None else None
+    print(f"[bench] generated in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    c = attn_case.to(dev)
+    max_p = int(attn_case.prefix_lens.max())
+    max_w = int(attn_case.window_lens.max())
+    out = torch.empty_like(c.q)
+    R = V = 0
+    if edit_case is not None:
+        logits = edit_case.logits.to(dev)
+        cur = edit_case.cur_tokens.to(dev)
+        R, V = logits.shape
+        eo = (torch.empty(R, dtype=torch.int32, device=dev), torch.empty(R, dtype=torch.float32, device=dev),
+              torch.empty(R, dtype=torch.uint8, device=dev))
+    torch.cuda.synchronize()
+
+    # A plain copy of known size, outside the timed region: its rocprofv3 counter
+    # readings calibrate the HBM byte counters of the other kernels.
+    calib = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    calib2 = torch.empty_like(calib)
+    calib2.copy_(calib)
+    torch.cuda.synchronize()
+    del calib, calib2
+
+    def attention():
+        mbe.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens,
+                             attn_case.block_size, out=out, max_prefix_len=max_p, max_window_len=max_w,
+                             kv_split_tokens=args.kv_split_tokens)
+
+    def edit():
+        mbe.edit_select(logits, cur, edit_case.threshold, out=eo)
+
+    for _ in range(args.warmup):
+        attention()
+        if edit_case is not None:
+            edit()
+    torch.cuda.synchronize()
+
+    n = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+    stream = torch.cuda.current_stream(dev)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(n):
+        ev[i][0].record(stream)
+        attention()
+        ev[i][1].record(stream)
+        if edit_case is not None:
+            edit()
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    t_attn = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) / 1e3
+    t_edit = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) / 1e3 if edit_case is not None else 0.0
+    t_step = float(np.mean([e[0].elapsed_time(e[2]) for e in ev])) / 1e3
+
+    flops, attn_bytes = attention_work(attn_case)
+    e_bytes = edit_bytes(R, V) if edit_case is not None else 0
+    sol = flops / (PEAK_BF16_TFLOPS * 1e12) + e_bytes / (PEAK_HBM_GBS * 1e9)
+    attn_tflops = flops / t_attn / 1e12
+    edit_gbs = e_bytes / t_edit / 1e9 if edit_case is not None else None
+
+    traffic = measured_traffic("window_attention", args.workload)
+    res = {
+        "metric": METRIC,
+        "value": round(100.0 * sol / t_step, 3),
+        "unit": "% of MI355X peak (speed-of-light step time / measured step time)",
+        "n_gpus": 1,
+        "steps": n,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) Q/K/V, N(0,3) logits with planted peaks; shuffled 16-token pages)",
+        "config": {
+            "workload": args.workload,
+            "batch": attn_case.batch,
+            "prefix_lens": [int(attn_case.prefix_lens.min()), int(attn_case.prefix_lens.max())],
+            "block_size": attn_case.block_size,
+            "window_blocks": max_w // attn_case.block_size,
+            "q_heads": attn_case.num_q_heads, "kv_heads": attn_case.num_kv_heads,
+            "head_dim": attn_case.head_dim, "page_size": 16, "mask": "bidirectional window",
+            "edit_rows": R if edit_case is not None else 0, "vocab": V if edit_case is not None else 0,
+            "kv_split_tokens": args.kv_split_tokens,
+        },
+        "attention": {"ms": round(t_attn * 1e3, 4), "tflops": round(attn_tflops, 2),
+                      "pct_mfma_peak": round(100 * attn_tflops / PEAK_BF16_TFLOPS, 2),
+                      "gflop": round(flops / 1e9, 2), "algorithmic_mb": round(attn_bytes / 1e6, 1)},
+        "edit_select": ({"ms": round(t_edit * 1e3, 4), "gbs": round(edit_gbs, 1),
+                         "pct_hbm_peak": round(100 * edit_gbs / PEAK_HBM_GBS, 2),
+                         "algorithmic_mb": round(e_bytes / 1e6, 1)} if edit_case is not None else None),
+        "roofline": {"kernel": "window_attention_kernel<128,0>", "bound": "mfma",
+                     "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic},
+        "wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline and edit_case is not None:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl, attn_case, edit_case, flops, e_bytes,
+                                           args.attn_sample, args.edit_sample)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

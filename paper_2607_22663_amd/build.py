@@ -16,10 +16,14 @@ LIB = os.path.join(PKG, "libmbe.so")
 SOURCES = ["abi.cpp", "edit_select.hip", "attn_window.hip"]
 
 # Packed fp32 VALU ops are disabled for every HIP source: ordinary float code
-# is compiled to scalar-per-lane v_*_f32 instructions only.
+# is compiled to scalar-per-lane v_*_f32 instructions only.  MFMA results are
+# allocated in ordinary VGPRs where possible (the softmax reads the score
+# accumulators with VALU instructions every tile; AGPR results would need a
+# copy each time).
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-result",
 ]
 

@@ -9,16 +9,15 @@
 // Work decomposition
 //   All G = Hq/Hkv query heads of a KV head share its keys, so the rows of
 //   one (sequence b, KV head g) are packed: row r = i*G + hl is window
-//   position i of query head g*G + hl.  A workgroup (4 waves) owns 256 such
-//   rows and one split of the key range; a wave owns 64 rows as two 32-row
-//   MFMA column blocks.
+//   position i of query head g*G + hl.  A workgroup (4 waves, one per SIMD)
+//   owns 256 such rows and one split of the key range; a wave owns 64 rows
+//   as two 32-row MFMA column blocks.
 //
 // Contractions on bf16 MFMA (v_mfma_f32_32x32x16_bf16)
 //   S^T = K . Q^T : A = 32 keys x 16 dims from LDS, B = Q^T from registers.
-//                  The result holds one query per lane (column), so the
-//                  softmax row statistics stay in the lane; only the two
-//                  32-lane halves, which hold different keys of the same
-//                  query, exchange the maximum once per tile.
+//                  The result holds one query per lane (column), so softmax
+//                  statistics stay in the lane; only the two 32-lane halves,
+//                  which hold different keys of the same query, exchange.
 //   O^T += V^T . P^T : A = 32 dims x 16 keys of V^T from LDS, B = P^T taken
 //                  straight from the S^T accumulators.  Keys are assigned to
 //                  MFMA rows through a fixed permutation (swap of bits 2 and 3
@@ -26,22 +25,33 @@
 //                  one P.V step are 8 consecutive keys: with token-minor V
 //                  pages that is one 16-byte LDS read per operand.
 //
-// Softmax: online, base 2, fp32.  The running maximum is only raised when a
-// tile exceeds it by more than 2^8 (decided per wave), so the O rescale is
-// skipped on most tiles; exponentials stay below 2^8.
+// Softmax: base 2, fp32, against a fixed reference per row instead of a
+// running maximum, so inside the key loop the O accumulators are touched by
+// MFMA only.  The reference is the row's maximum over its first key tile.
+// Later exponentials 2^(s - ref) may exceed 1; bf16 P and fp32 sums share
+// fp32's exponent range, so nothing overflows unless a later score exceeds
+// the reference by about 2^127.  The row sum is checked once at the end of
+// the key range: if any sum exceeds 2^64 (or is not finite) the workgroup
+// makes a max-only run over its keys and then a full run with the true
+// maximum as reference, where no exponential exceeds 1.
 //
 // Split-KV: long prefixes are cut into kv_chunk-key splits.  Each split
-// writes unnormalised O, its maximum and its sum; the last split of a query
-// tile to finish (atomic arrival counter, reset after use) merges them in
-// split order: M = max m_s, O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s.
+// writes unnormalised O, its reference and its sum; the last split of a
+// query tile to finish (atomic arrival counter, reset after use) merges them
+// in split order: M = max m_s, O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s.
 //
-// K/V tiles of 64 keys (four 16-token pages, gathered through the page table)
-// are staged in LDS with a register-prefetch double buffer and padded rows
-// (no bank conflicts on the 16-byte operand reads).  Workgroup ids are mapped
-// so that each XCD runs a contiguous range of work units and the query tiles
-// that share a key range run back to back on the same XCD (shared L2).
+// K/V tiles of 64 keys (four 16-token pages gathered through the page table)
+// go from HBM straight into LDS (global_load_lds_dwordx4, no registers),
+// double buffered.  Each wave instruction fills 1 KB of LDS; the lanes fetch
+// their 16-byte chunks in an XOR-swizzled order, so the global reads stay
+// contiguous per page while the MFMA operand reads are free of bank
+// conflicts.  Workgroup ids are mapped so that each XCD runs a contiguous
+// range of work units and the query tiles sharing a key range run back to
+// back on the same XCD (shared L2).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "internal.h"
 
@@ -50,28 +60,36 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kT = kWaves * 64;
 constexpr float kNegInf = -INFINITY;
-constexpr float kLazyRescale = 8.0f;   // log2 units
+constexpr float kSumLimit = 0x1p64f;   // row sums above this trigger the exact rerun
 
 template <int D>
-struct Lds {
-  static constexpr int kStride = D + 8;          // K row: 64 keys x (D + 8) bf16
-  static constexpr int vStride = kKeyTile + 8;   // V^T row: D dims x (64 + 8) bf16
-  static constexpr int kElems = kKeyTile * kStride;
-  static constexpr int vElems = D * vStride;
-  static constexpr int bufElems = kElems + vElems;
-  static constexpr int bytes = 2 * bufElems * 2;   // double buffer
+struct Tile {
+  static constexpr int kRowChunks = D / 8;                   // 16-byte chunks per K row
+  static constexpr int kKBytes = kKeyTile * D * 2;           // K: 64 keys x D
+  static constexpr int kVBytes = D * kKeyTile * 2;           // V^T: D dims x 64 keys
+  static constexpr int kBufBytes = kKBytes + kVBytes;
+  static constexpr int kLoads = kKeyTile * D / 8 / kT;       // direct loads per thread per tile (K and V each)
 };
+
+// LDS chunk position of global chunk j of K row r (XOR swizzle; an involution).
+template <int D>
+__device__ __forceinline__ int k_swz(int r) {
+  return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+// LDS chunk position of key chunk ci (8 keys) of V^T row d.
+__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 7; }
 
 // Bit swap 2<->3 of a row index in 0..31: MFMA row -> key within a 32-key block.
 __device__ __forceinline__ int perm_row(int r) {
   return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two floats to two bf16, round to nearest even (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -79,77 +97,92 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ bf16x8 lds_read8(const uint16_t *p) {
-  return *reinterpret_cast<const bf16x8 *>(p);
+// s_waitcnt immediate that waits for vector-memory count <= n only
+// (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt fields at their maxima).
+constexpr int wait_vmcnt(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+
+// Workgroup barrier for LDS only, without the memory fence of
+// __syncthreads(): that fence would also wait for every direct HBM->LDS load
+// still in flight.  The caller first waits for the loads it needs; pending
+// LDS writes of this wave are waited for here.  The memory clobber keeps the
+// compiler from moving LDS accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ __forceinline__ bf16x8 lds_read8(const char *base, int byte_off) {
+  return *reinterpret_cast<const bf16x8 *>(base + byte_off);
 }
 
+typedef const __attribute__((address_space(4))) int32_t const_i32;
+
+// Page ids of the four pages of the 64-key tile starting at key0, read with
+// scalar loads (the page table is constant during the kernel).  Slots past
+// the table row are clamped into it and ids into the pool; such pages only
+// feed keys that are masked and whose V rows are zeroed.
+__device__ __forceinline__ void tile_pages(const AttnParams &p, int b, int key0, int (&pid)[4]) {
+  const_i32 *row = (const_i32 *)(p.page_table) + static_cast<int64_t>(b) * p.max_pages;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int slot = min(key0 / kPageSize + q, p.max_pages - 1);
+    pid[q] = min(max(row[slot], 0), p.num_pages - 1);
+  }
+}
+
+// Issues the direct HBM->LDS loads of one 64-key tile (K and V) into `buf`.
 template <int D>
-struct TileLoader {
-  // chunks of 8 bf16 (16 bytes): a page holds 2*D chunks of K and 2*D of V
-  static constexpr int kChunksPerPage = 2 * D;
-  static constexpr int kPagesPerPass = kT / kChunksPerPage;   // 1 (D=128) or 2 (D=64)
-  static constexpr int kPasses = (kKeyTile / kPageSize) / kPagesPerPass;
-  uint4 k[kPasses];
-  uint4 v[kPasses];
-  int vvalid[kPasses];      // valid slots of this page for V zero fill (16 = all)
-
-  __device__ __forceinline__ void load(const AttnParams &p, int b, int g, int tile_key0, int n_all) {
-    const int tid = threadIdx.x;
-    const int c = tid % kChunksPerPage;
+__device__ __forceinline__ void load_tile(const AttnParams &p, int g, const int (&pid)[4], char *buf) {
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  constexpr int RC = Tile<D>::kRowChunks;
 #pragma unroll
-    for (int j = 0; j < kPasses; ++j) {
-      const int pg = j * kPagesPerPass + tid / kChunksPerPage;     // page within tile
-      const int tok0 = tile_key0 + pg * kPageSize;
-      if (tok0 < n_all) {
-        const int slot_in_table = min(tok0 / kPageSize, p.max_pages - 1);
-        int page = p.page_table[static_cast<int64_t>(b) * p.max_pages + slot_in_table];
-        page = min(max(page, 0), p.num_pages - 1);
-        const int64_t base = (static_cast<int64_t>(page) * p.num_kv_heads + g) * (kPageSize * D);
-        k[j] = *reinterpret_cast<const uint4 *>(p.k_pages + base + c * 8);
-        v[j] = *reinterpret_cast<const uint4 *>(p.v_pages + base + c * 8);
-        vvalid[j] = min(kPageSize, n_all - tok0);
-      } else {
-        k[j] = make_uint4(0, 0, 0, 0);
-        v[j] = make_uint4(0, 0, 0, 0);
-        vvalid[j] = 0;
-      }
+  for (int j = 0; j < Tile<D>::kLoads; ++j) {
+    const int inst = wave * Tile<D>::kLoads + j;      // which 1 KB of the tile
+    const int s = inst * 64 + lane;                   // LDS chunk slot of this lane
+    // K: slot s holds chunk (s % RC) ^ swz of key row s / RC
+    {
+      const int row = s / RC;
+      const int chunk = (s % RC) ^ k_swz<D>(row);
+      const int64_t src = (static_cast<int64_t>(pid[row >> 4]) * p.num_kv_heads + g) * (kPageSize * D) +
+                          (row & 15) * D + chunk * 8;
+      __builtin_amdgcn_global_load_lds(p.k_pages + src, (lds_void *)(buf + inst * 1024), 16, 0, 0);
+    }
+    // V^T: slot s holds key chunk (s % 8) ^ swz of dim row s / 8
+    {
+      const int d = s >> 3;
+      const int ci = (s & 7) ^ v_swz(d);                // keys 8ci .. 8ci+7 of the tile
+      const int64_t src = (static_cast<int64_t>(pid[ci >> 1]) * p.num_kv_heads + g) * (kPageSize * D) +
+                          d * kPageSize + (ci & 1) * 8;
+      __builtin_amdgcn_global_load_lds(p.v_pages + src,
+                                       (lds_void *)(buf + Tile<D>::kKBytes + inst * 1024), 16, 0, 0);
     }
   }
+}
 
-  __device__ __forceinline__ void store(uint16_t *buf) const {
-    const int tid = threadIdx.x;
-    const int c = tid % kChunksPerPage;
-    uint16_t *ks = buf;
-    uint16_t *vs = buf + Lds<D>::kElems;
+// Zeroes V^T entries of keys at or past `nvalid` (tile-relative) so that
+// unread page tails (which may hold anything) cannot reach the P.V product.
+template <int D>
+__device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
+  uint16_t *vs = reinterpret_cast<uint16_t *>(buf + Tile<D>::kKBytes);
+  for (int s = threadIdx.x; s < D * 8; s += kT) {
+    const int d = s >> 3;
+    const int ci = (s & 7) ^ v_swz(d);
+    const int k0 = ci * 8;
+    if (k0 + 8 <= nvalid) continue;
+    uint16_t *e = vs + s * 8;
 #pragma unroll
-    for (int j = 0; j < kPasses; ++j) {
-      const int pg = j * kPagesPerPass + tid / kChunksPerPage;
-      // K page: [16 slots][D]; chunk c = slot * (D/8) + d/8
-      const int slot = c / (D / 8);
-      const int d0 = (c % (D / 8)) * 8;
-      *reinterpret_cast<uint4 *>(ks + (pg * kPageSize + slot) * Lds<D>::kStride + d0) = k[j];
-      // V page: [D][16 slots]; chunk c = d * 2 + half
-      const int d = c / 2;
-      const int s0 = (c % 2) * 8;
-      uint4 w = v[j];
-      const int nv = vvalid[j] - s0;    // valid slots within this 8-slot chunk
-      if (nv < 8) {
-        uint32_t *ww = reinterpret_cast<uint32_t *>(&w);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint32_t lo_keep = (2 * e < nv) ? 0x0000ffffu : 0u;
-          const uint32_t hi_keep = (2 * e + 1 < nv) ? 0xffff0000u : 0u;
-          ww[e] &= (lo_keep | hi_keep);
-        }
-      }
-      *reinterpret_cast<uint4 *>(vs + d * Lds<D>::vStride + pg * kPageSize + s0) = w;
-    }
+    for (int k = 0; k < 8; ++k)
+      if (k0 + k >= nvalid) e[k] = 0;
   }
-};
+}
 
 template <int D, int MODE>
 __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
-  __shared__ __align__(16) uint16_t lds[2 * Lds<D>::bufElems];
+  // four K/V tile buffers (separate objects, so the compiler can tell which
+  // in-flight direct loads a read depends on), three tiles in flight
+  __shared__ __align__(1024) char lds0[Tile<D>::kBufBytes];
+  __shared__ __align__(1024) char lds1[Tile<D>::kBufBytes];
+  __shared__ __align__(1024) char lds2[Tile<D>::kBufBytes];
+  __shared__ __align__(1024) char lds3[Tile<D>::kBufBytes];
   __shared__ uint32_t sh_last;
 
   // ---- work unit: XCD-contiguous ranges of (bg, split, qtile) with qtile fastest
@@ -234,120 +267,229 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
         qreg[qb][kk] = bf16x8{};
     }
 
+  // ---- loop-invariant LDS operand offsets of this lane
+  // K: row perm_row(c) (+32 for the second key block), chunk 2kk + h
+  const int krow = perm_row(c);
+  int koff[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) koff[kk] = krow * (2 * D) + (((2 * kk + h) ^ k_swz<D>(krow)) << 4);
+  // V^T: row c (+32 per dim block), key chunk 4kbk + 2mm + h
+  int voff[2][2];
+#pragma unroll
+  for (int kbk = 0; kbk < 2; ++kbk)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+      voff[kbk][mm] = Tile<D>::kKBytes + c * (kKeyTile * 2) + (((4 * kbk + 2 * mm + h) ^ v_swz(c)) << 4);
+
   constexpr int DB = D / 32;
   f32x16 acc_o[2][DB];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc_o[qb][db] = f32x16{};
-  float m_run[2] = {kNegInf, kNegInf};   // log2 units
+  float m_ref[2] = {kNegInf, kNegInf};   // reference, log2 units
   float l_run[2] = {0.f, 0.f};
 
-  // key offset (within a 32-key block) held in accumulator register v
-  // of this lane: 16*(v>>3) + 8h + (v&7)
-  const int prow = perm_row(c);
+  // rows of this workgroup see keys [kb, lim); lim is smallest for the first
+  // row, so tiles ending at or below it need no mask for any row
+  int wg_min = ke;
+  if (MODE == 1) wg_min = min(ke, P + ((row0 / G) / p.block_size + 1) * p.block_size);
+  const int t_full = min(ntiles, max(0, (wg_min - kb) / kKeyTile));
 
-  TileLoader<D> ld;
-  if (ntiles > 0) {
-    ld.load(p, b, g, kb, n_all);
-    ld.store(lds);
-  }
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const uint16_t *buf = lds + (t & 1) * Lds<D>::bufElems;
-    const uint16_t *ks = buf;
-    const uint16_t *vs = buf + Lds<D>::kElems;
-    const int key0 = kb + t * kKeyTile;
-    const bool more = t + 1 < ntiles;
-    if (more) ld.load(p, b, g, key0 + kKeyTile, n_all);
-
-    // S^T = K . Q^T for two 32-key blocks x two 32-query blocks
-    f32x16 s[2][2];
+  // S^T of one 32-key block for both query blocks: operands first, then MFMA
+  auto qk_block = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
+    bf16x8 a[KK];
 #pragma unroll
-    for (int kbk = 0; kbk < 2; ++kbk) {
-      s[kbk][0] = f32x16{};
-      s[kbk][1] = f32x16{};
-      const uint16_t *krow = ks + (kbk * 32 + prow) * Lds<D>::kStride + h * 8;
+    for (int kk = 0; kk < KK; ++kk) a[kk] = lds_read8(buf, koff[kk] + kbk * 32 * (2 * D));
+    sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[0][0], f32x16{}, 0, 0, 0);
+    sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[1][0], f32x16{}, 0, 0, 0);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const bf16x8 a = lds_read8(krow + kk * 16);
-        s[kbk][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[0][kk], s[kbk][0], 0, 0, 0);
-        s[kbk][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[1][kk], s[kbk][1], 0, 0, 0);
+    for (int kk = 1; kk < KK; ++kk) {
+      sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[0][kk], sc[0], 0, 0, 0);
+      sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[1][kk], sc[1], 0, 0, 0);
+    }
+  };
+  // keys at or past a row's limit get -inf
+  auto mask_block = [&](int kblk0, f32x16 (&sc)[2]) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = kblk0 + 16 * (v >> 3) + 8 * h + (v & 7);
+        if (key >= lim[qb]) sc[qb][v] = kNegInf;
       }
-    }
-
-    // mask (only on tiles that reach past some row's limit)
-    if (key0 + kKeyTile > wmin) {
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int kbk = 0; kbk < 2; ++kbk)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = key0 + kbk * 32 + 16 * (v >> 3) + 8 * h + (v & 7);
-            if (key >= lim[qb]) s[kbk][qb][v] = kNegInf;
-          }
-    }
-
-    // online softmax; P^T packed to bf16 in MFMA-B layout
-    uint32_t pk[2][2][2][4];    // [qb][kbk][m][4 dwords = 8 bf16]
+  };
+  auto max_block = [&](f32x16 (&sc)[2]) {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       float mx = kNegInf;
 #pragma unroll
-      for (int kbk = 0; kbk < 2; ++kbk)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kbk][qb][v]);
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[qb][v]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mt = mx * p.scale_log2;
-      const bool need = mt > m_run[qb] + kLazyRescale;
-      if (__any(need)) {
-        const float mnew = fmaxf(m_run[qb], mt);
-        const float alpha = (mnew == kNegInf) ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - mnew);
-        l_run[qb] *= alpha;
+      m_ref[qb] = fmaxf(m_ref[qb], mx * p.scale_log2);
+    }
+  };
+  // numerators 2^(s*scale*log2e - ref) to bf16 P^T, then O^T += V^T . P^T
+  auto softmax_pv = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
+    bf16x8 va[2][DB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) acc_o[qb][db] *= alpha;
-        m_run[qb] = mnew;
-      }
-      const float msafe = (m_run[qb] == kNegInf) ? 0.f : m_run[qb];
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) va[mm][db] = lds_read8(buf, voff[kbk][mm] + db * 32 * (kKeyTile * 2));
+    bf16x8 pb[2][2];    // [qb][m]: keys 16m + 8h .. +7 of this block
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float msafe = (m_ref[qb] == kNegInf) ? 0.f : m_ref[qb];
+      float e[16];
       float lsum = 0.f;
 #pragma unroll
-      for (int kbk = 0; kbk < 2; ++kbk) {
-        float e[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kbk][qb][v], p.scale_log2, -msafe));
-          lsum += e[v];
-        }
-#pragma unroll
-        for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4)
-            pk[qb][kbk][mm][q4] = pack_bf16x2(e[8 * mm + 2 * q4], e[8 * mm + 2 * q4 + 1]);
+      for (int v = 0; v < 16; ++v) {
+        e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][v], p.scale_log2, -msafe));
+        lsum += e[v];
       }
       l_run[qb] += lsum;
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm) {
+        const u32x4 w = {pack_bf16x2(e[8 * mm + 0], e[8 * mm + 1]), pack_bf16x2(e[8 * mm + 2], e[8 * mm + 3]),
+                         pack_bf16x2(e[8 * mm + 4], e[8 * mm + 5]), pack_bf16x2(e[8 * mm + 6], e[8 * mm + 7])};
+        pb[qb][mm] = __builtin_bit_cast(bf16x8, w);
+      }
     }
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        acc_o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[0][mm], acc_o[0][db], 0, 0, 0);
+        acc_o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[1][mm], acc_o[1][db], 0, 0, 0);
+      }
+  };
+  // ---- key loop: tile t lives in buffer t % 4; tiles t+1..t+3 are in flight
+  // while tile t is computed.  pid holds the page ids of the next tile to load.
+  int pid[4];
+  auto buf_of = [&](int t) -> char * {
+    switch (t & 3) {
+      case 0: return lds0;
+      case 1: return lds1;
+      case 2: return lds2;
+      default: return lds3;
+    }
+  };
+  // direct loads of tile t into dst, then the page ids of tile t + 1
+  auto issue = [&](int t, char *dst) {
+    load_tile<D>(p, g, pid, dst);
+    tile_pages(p, b, kb + (t + 1) * kKeyTile, pid);
+  };
+  constexpr int kLoadsPerTile = 2 * Tile<D>::kLoads;     // direct loads per thread per tile
+  // waits until at most n tiles' loads of this thread are still in flight,
+  // then meets the other waves: afterwards every earlier tile is in LDS
+  auto land = [&](int n) {
+    if (n >= 2) __builtin_amdgcn_s_waitcnt(wait_vmcnt(2 * kLoadsPerTile));
+    else if (n == 1) __builtin_amdgcn_s_waitcnt(wait_vmcnt(kLoadsPerTile));
+    else __builtin_amdgcn_s_waitcnt(wait_vmcnt(0));
+    lds_barrier();
+  };
+  // V rows of keys past n_all in tile t (only the last tile can have them)
+  auto fix_tail = [&](int t) {
+    const int key0 = kb + t * kKeyTile;
+    if (key0 + kKeyTile > n_all) {
+      zero_v_tail<D>(buf_of(t), n_all - key0);
+      lds_barrier();
+    }
+  };
+  auto prologue = [&]() {
+    tile_pages(p, b, kb, pid);
+    for (int t = 0; t < 3 && t < ntiles; ++t) issue(t, buf_of(t));
+    land(min(2, ntiles - 1));
+    fix_tail(0);
+  };
+  auto compute = [&](const char *buf, int t, auto masked) {
+    const int key0 = kb + t * kKeyTile;
+    f32x16 s0[2], s1[2];
+    qk_block(buf, 0, s0);
+    qk_block(buf, 1, s1);
+    if constexpr (decltype(masked)::value) {
+      mask_block(key0, s0);
+      mask_block(key0 + 32, s1);
+    }
+    softmax_pv(buf, 0, s0);
+    softmax_pv(buf, 1, s1);
+  };
+  // one tile through dynamically chosen buffers (remainder, masked tiles)
+  auto generic_step = [&](int t, bool masked) {
+    if (t + 3 < ntiles) issue(t + 3, buf_of(t + 3));
+    if (masked) compute(buf_of(t), t, std::true_type{});
+    else compute(buf_of(t), t, std::false_type{});
+    if (t + 1 < ntiles) {
+      land(min(2, ntiles - 2 - t));
+      fix_tail(t + 1);
+    }
+  };
 
-    // O^T += V^T . P^T
+  // Run 0 takes the reference from the first 32-key block.  Run 1 happens
+  // only if some row sum left the safe range: it first finds the true row
+  // maxima with a K.Q-only pass, then repeats the full pass.
+  for (int run = 0; run < 2; ++run) {
+    if (ntiles > 0) {
+      if (run == 1) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const uint16_t *vrow = vs + (db * 32 + c) * Lds<D>::vStride + h * 8;
-#pragma unroll
-      for (int kbk = 0; kbk < 2; ++kbk)
-#pragma unroll
-        for (int mm = 0; mm < 2; ++mm) {
-          const bf16x8 a = lds_read8(vrow + kbk * 32 + mm * 16);
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) {
-            const bf16x8 bq = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(pk[qb][kbk][mm]));
-            acc_o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bq, acc_o[qb][db], 0, 0, 0);
+        for (int qb = 0; qb < 2; ++qb) m_ref[qb] = kNegInf;
+        prologue();
+        for (int t = 0; t < ntiles; ++t) {
+          if (t + 3 < ntiles) issue(t + 3, buf_of(t + 3));
+          const char *buf = buf_of(t);
+          const int key0 = kb + t * kKeyTile;
+          f32x16 s0[2], s1[2];
+          qk_block(buf, 0, s0);
+          qk_block(buf, 1, s1);
+          mask_block(key0, s0);
+          mask_block(key0 + 32, s1);
+          max_block(s0);
+          max_block(s1);
+          if (t + 1 < ntiles) {
+            land(min(2, ntiles - 2 - t));
+            fix_tail(t + 1);
           }
         }
+        lds_barrier();
+      }
+      prologue();
+      if (run == 0) {
+        f32x16 sc[2];
+        qk_block(lds0, 0, sc);
+        mask_block(kb, sc);
+        max_block(sc);
+      }
     }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc_o[qb][db] = f32x16{};
+      l_run[qb] = 0.f;
+    }
+    int t = 0;
+    // unmasked tiles, four per iteration through fixed buffers; every tile
+    // loaded here exists, so two tiles stay in flight at each barrier
+    for (; t + 6 < ntiles && t + 3 < t_full; t += 4) {
+      issue(t + 3, lds3);
+      compute(lds0, t, std::false_type{});
+      land(2);
+      issue(t + 4, lds0);
+      compute(lds1, t + 1, std::false_type{});
+      land(2);
+      issue(t + 5, lds1);
+      compute(lds2, t + 2, std::false_type{});
+      land(2);
+      issue(t + 6, lds2);
+      compute(lds3, t + 3, std::false_type{});
+      land(2);
+    }
+    for (; t < ntiles; ++t) generic_step(t, t >= t_full);
+    if (ntiles > 0) lds_barrier();      // all waves done with the buffers
 
-    if (more) ld.store(lds + ((t + 1) & 1) * Lds<D>::bufElems);
-    __syncthreads();
+    if (run == 1) break;
+    bool bad = false;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float lt = l_run[qb] + __shfl_xor(l_run[qb], 32);
+      bad |= valid[qb] && !(lt <= kSumLimit);
+    }
+    if (!__syncthreads_or(bad)) break;
   }
 
   // ---- epilogue
@@ -393,7 +535,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       }
     if (h == 0) {
       float *pml = p.part_ml + (split * split_stride + rowidx) * 2;
-      *reinterpret_cast<float2 *>(pml) = make_float2(m_run[qb], l_tot[qb]);
+      *reinterpret_cast<float2 *>(pml) = make_float2(m_ref[qb], l_tot[qb]);
     }
   }
   __threadfence();

@@ -20,15 +20,20 @@ Layouts produced (all row-major, contiguous):
   logits     bf16  [rows, vocab]
   cur_tokens int32 [rows]
 
-Draw order per attention case (numpy PCG64 keyed by (seed, 0)): prefix
-lengths, Q, K, V (fp32 N(0,1) rounded to bf16 RNE), page permutation.
-Per edit case (keyed by (seed, 1)): logits (fp32 N(0, sigma) -> bf16),
-planted rows and columns, current tokens.
+Random streams: numpy PCG64 keyed by (seed, case kind, tensor tag, chunk).
+Attention case (kind 0): prefix lengths and the page permutation from tag 0;
+Q, K, V from tags 1, 2, 3 as fp32 N(0,1) rounded to bf16 (RNE).  Edit case
+(kind 1): logits from tag 1 as fp32 N(0, sigma) rounded to bf16; planted rows
+and columns and current tokens from tag 0.  Large tensors are drawn in
+2^22-element chunks, each from its own keyed stream, so several threads can
+fill them and the values do not depend on the thread count.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import math
+import os
 from typing import Optional
 
 import numpy as np
@@ -92,26 +97,34 @@ WORKLOADS = {
 SPAN_SWEEP_K = (1, 2, 4, 8)
 
 
-def _rng(seed: int, stream: int) -> np.random.Generator:
-    return np.random.Generator(np.random.PCG64([int(seed), int(stream)]))
+_CHUNK = 1 << 22
+_THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
-def _to_bf16(x: np.ndarray) -> torch.Tensor:
-    """fp32 numpy -> bf16 torch (round to nearest even, done by torch on CPU)."""
-    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
+def _rng(seed: int, kind: int, tag: int = 0, chunk: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64([int(seed), int(kind), int(tag), int(chunk)]))
 
 
-def _normal_bf16(rng: np.random.Generator, shape, scale: float = 1.0,
-                 chunk: int = 1 << 24) -> torch.Tensor:
-    """N(0, scale) drawn in fp32 in fixed-size chunks, rounded to bf16."""
+def _normal_bf16(seed: int, kind: int, tag: int, shape, scale: float = 1.0) -> torch.Tensor:
+    """N(0, scale) drawn in fp32 chunk by chunk (one keyed stream per chunk),
+    rounded to bf16 (round to nearest even, by torch on the CPU)."""
     n = int(np.prod(shape))
     out = torch.empty(n, dtype=torch.bfloat16)
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
-        x = rng.standard_normal(e - s, dtype=np.float32)
+
+    def fill(i):
+        s, e = i * _CHUNK, min(n, (i + 1) * _CHUNK)
+        x = _rng(seed, kind, tag, i).standard_normal(e - s, dtype=np.float32)
         if scale != 1.0:
             x *= np.float32(scale)
-        out[s:e] = _to_bf16(x)
+        out[s:e] = torch.from_numpy(x).to(torch.bfloat16)
+
+    nchunks = (n + _CHUNK - 1) // _CHUNK
+    if nchunks <= 1:
+        for i in range(nchunks):
+            fill(i)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(_THREADS) as ex:
+            list(ex.map(fill, range(nchunks)))
     return out.view(*shape)
 
 
@@ -178,12 +191,12 @@ def make_attention_case(spec: AttnSpec, seed: int, *,
     B = spec.block_size
     Hq, Hkv, D = spec.num_q_heads, spec.num_kv_heads, spec.head_dim
     total_q = int(W.sum())
-    q = _normal_bf16(rng, (total_q, Hq, D), scale=q_scale)
+    q = _normal_bf16(seed, 0, 1, (total_q, Hq, D), scale=q_scale)
     n_tok = P.astype(np.int64) + W
     n_pages = (n_tok + PAGE_SIZE - 1) // PAGE_SIZE
     num_pages = int(n_pages.sum()) + int(extra_pages)
-    k_pages = _normal_bf16(rng, (num_pages, Hkv, PAGE_SIZE, D))
-    v_pages = _normal_bf16(rng, (num_pages, Hkv, D, PAGE_SIZE))
+    k_pages = _normal_bf16(seed, 0, 2, (num_pages, Hkv, PAGE_SIZE, D))
+    v_pages = _normal_bf16(seed, 0, 3, (num_pages, Hkv, D, PAGE_SIZE))
     perm = rng.permutation(num_pages).astype(np.int32)
     max_pages = max(1, int(n_pages.max()) if len(n_pages) else 1)
     page_table = np.zeros((P.shape[0], max_pages), dtype=np.int32)
@@ -232,7 +245,7 @@ def make_edit_case(spec: EditSpec, seed: int, *, rows: Optional[int] = None,
     rng = _rng(seed, 1)
     R = spec.rows if rows is None else int(rows)
     V = spec.vocab
-    logits = _normal_bf16(rng, (R, V), scale=spec.sigma)
+    logits = _normal_bf16(seed, 1, 1, (R, V), scale=spec.sigma)
     n_plant = int(math.floor(R * spec.planted_fraction))
     prow = np.sort(rng.choice(R, size=n_plant, replace=False)) if n_plant else np.zeros(0, np.int64)
     pcol = rng.integers(0, V, size=n_plant)
