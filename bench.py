@@ -159,6 +159,7 @@ def main():
     c = attn_case.to(dev)
     max_p = int(attn_case.prefix_lens.max())
     max_w = int(attn_case.window_lens.max())
+    hp, hw = attn_case.prefix_lens, attn_case.window_lens      # host copies of the lengths
     out = torch.empty_like(c.q)
     R = V = 0
     if edit_case is not None:
@@ -180,7 +181,7 @@ def main():
     def attention():
         mbe.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens,
                              attn_case.block_size, out=out, max_prefix_len=max_p, max_window_len=max_w,
-                             kv_split_tokens=args.kv_split_tokens)
+                             kv_split_tokens=args.kv_split_tokens, host_prefix_lens=hp, host_window_lens=hw)
 
     def edit():
         mbe.edit_select(logits, cur, edit_case.threshold, out=eo)

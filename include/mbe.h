@@ -24,6 +24,8 @@
  *     error string in mbe_last_error().
  *   - No global mutable state except the thread-local error string.  Calls
  *     that share a workspace must not overlap in time.
+ *   - One call launches one kernel, plus a small merge/finalize kernel when
+ *     the work is split across workgroups (see the workspace sizes).
  */
 #ifndef MBE_H_
 #define MBE_H_
@@ -89,12 +91,16 @@ typedef struct {
   float softmax_scale;        /* <= 0 selects 1/sqrt(head_dim)                      */
   int32_t kv_split_tokens;    /* keys per split-KV chunk; 0 lets the library choose;
                                  otherwise a positive multiple of 64                 */
-  void *workspace;            /* device memory of mbe_window_attention_workspace_size
-                                 bytes, 256-byte aligned, zero-filled before its first
-                                 use (see mbe_workspace_zero).  Its first 64 KB hold
-                                 arrival counters that every call leaves at zero;
-                                 results go after them, so one workspace serves calls
-                                 of any shape that fit in it                         */
+  const int32_t *host_prefix_lens;  /* optional HOST copies of prefix_lens /         */
+  const int32_t *host_window_lens;  /* window_lens ([batch] each, NULL = unknown).
+                                 They are read on the host only, to size the
+                                 split-KV chunks from the total work and to start
+                                 the longest sequences first; they must equal the
+                                 device values.  Ignored when batch > 1024.          */
+  void *workspace;            /* device memory of at least
+                                 mbe_window_attention_workspace_size bytes, 256-byte
+                                 aligned, any contents (split-KV partial results);
+                                 may be NULL when that size is 0                     */
   size_t workspace_bytes;
   void *stream;               /* hipStream_t                                        */
 } mbe_attn_opts;
@@ -125,10 +131,11 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
                                      const int32_t *page_table, const int32_t *prefix_lens,
                                      int32_t block_size, void *out, const mbe_attn_opts *opts);
 
-/* Workspace bytes the attention calls need for these shapes and options:
- * 64 KB of arrival counters (one per 256-row query tile, at most 16384 tiles
- * when the key range is split) plus the split-KV partial results.  0 means
- * the plan needs no split and no workspace.
+/* Workspace bytes the attention calls need for these shapes and options
+ * (all of opts, host lengths included, since they shape the split plan): the
+ * split-KV partial results.  0 means the plan needs no split and no
+ * workspace.  When some sequence is split, the call runs a second, small
+ * kernel that merges the partial results.
  * Returns (size_t)-1 if the arguments are invalid. */
 size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv,
                                            const mbe_attn_opts *opts, int32_t block_size);
@@ -143,8 +150,8 @@ size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv,
  * NaN or all -inf rows are outside the contract.  Accumulation is fp32; conf
  * is a correctly rounded reciprocal.  Deterministic: the same inputs give
  * bitwise the same outputs.  workspace: mbe_edit_select_workspace_size bytes,
- * 256-byte aligned, zero-filled before first use; its first 64 KB are arrival
- * counters that every call leaves at zero (may be NULL when the size is 0).
+ * 256-byte aligned, any contents (per-chunk partial results when a row is
+ * reduced by several workgroups; may be NULL when the size is 0).
  * Returns MBE_OK with no launch when rows is 0; MBE_ERR_BAD_VALUE for a NaN
  * threshold. */
 mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
@@ -155,10 +162,6 @@ mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int6
 /* Workspace bytes mbe_edit_select needs for rows x vocab (0 = none).
  * Returns (size_t)-1 for negative sizes. */
 size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab);
-
-/* Zero-fills `bytes` bytes of a workspace on `stream` with a kernel (no
- * hipMemset), e.g. once after allocating it. */
-mbe_status mbe_workspace_zero(void *workspace, size_t bytes, void *stream);
 
 /* Static description of a status code. */
 const char *mbe_status_string(mbe_status s);

@@ -26,8 +26,7 @@ STATUS_NAMES = {0: "MBE_OK", 1: "MBE_ERR_NULL_ARG", 2: "MBE_ERR_BAD_SHAPE", 3: "
 MASK_MODES = {"bidir": 0, "block_causal": 1}
 
 EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
-           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_workspace_zero",
-           "mbe_status_string", "mbe_last_error")
+           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_status_string", "mbe_last_error")
 
 
 class MbeError(RuntimeError):
@@ -47,7 +46,8 @@ class AttnOpts(ctypes.Structure):
                 ("max_pages_per_seq", ctypes.c_int32), ("total_q", ctypes.c_int32),
                 ("max_prefix_len", ctypes.c_int32), ("max_window_len", ctypes.c_int32),
                 ("mask_mode", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-                ("kv_split_tokens", ctypes.c_int32), ("workspace", ctypes.c_void_p),
+                ("kv_split_tokens", ctypes.c_int32), ("host_prefix_lens", ctypes.c_void_p),
+                ("host_window_lens", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
                 ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p)]
 
 
@@ -82,8 +82,6 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_edit_select.restype = ctypes.c_int
         lib.mbe_edit_select_workspace_size.argtypes = [i64, i64]
         lib.mbe_edit_select_workspace_size.restype = sz
-        lib.mbe_workspace_zero.argtypes = [vp, sz, vp]
-        lib.mbe_workspace_zero.restype = ctypes.c_int
         lib.mbe_status_string.argtypes = [ctypes.c_int]
         lib.mbe_status_string.restype = ctypes.c_char_p
         lib.mbe_last_error.argtypes = []
@@ -117,16 +115,14 @@ def _need(t: torch.Tensor, name: str, dtype, device, ndim=None):
 _workspaces = {}
 
 
-def _workspace(kind: str, device: torch.device, nbytes: int, stream) -> Optional[torch.Tensor]:
-    """Per-(kind, device) workspace, grown on demand and zero-filled by the
-    library when (re)allocated; every call leaves it ready for the next."""
+def _workspace(kind: str, device: torch.device, nbytes: int) -> Optional[torch.Tensor]:
+    """Per-(kind, device) workspace, grown on demand (contents do not matter)."""
     if nbytes == 0:
         return None
     key = (kind, device.index)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
-        _check("mbe_workspace_zero", load().mbe_workspace_zero(_ptr(ws), nbytes, stream))
         _workspaces[key] = ws
     return ws
 
@@ -160,30 +156,50 @@ def _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out):
     return kv, out
 
 
+def _host_i32(x, batch, name):
+    """A contiguous host int32 copy (kept alive by the caller) or None."""
+    if x is None:
+        return None
+    a = torch.as_tensor(x, dtype=torch.int32, device="cpu").contiguous()
+    if a.numel() != batch:
+        raise ValueError(f"{name} must have {batch} entries")
+    return a
+
+
 def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size, *,
                      out=None, mask_mode="bidir", softmax_scale=None, max_prefix_len=None,
-                     max_window_len=None, kv_split_tokens=0):
+                     max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None):
     """MBE editing-window attention (paper, Sec. "Training-Free MBE Decoding",
-    Eq. (4)).  Layouts as in include/mbe.h.  max_prefix_len / max_window_len
-    are host-side bounds; when omitted they are read from the device tensors
-    (a synchronisation)."""
+    Eq. (4)).  Layouts as in include/mbe.h.
+
+    max_prefix_len / max_window_len are host-side bounds.  host_prefix_lens /
+    host_window_lens are optional host copies of the lengths (they let the
+    library size splits from the total work and start long sequences first).
+    When neither bounds nor host lengths are given, the lengths are copied
+    from the device (a synchronisation)."""
     lib = load()
     kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
     _need(window_lens, "window_lens", torch.int32, q.device, 1)
     batch = prefix_lens.shape[0]
+    if max_prefix_len is None and host_prefix_lens is None:
+        host_prefix_lens = prefix_lens.cpu()
+    if max_window_len is None and host_window_lens is None:
+        host_window_lens = window_lens.cpu()
+    hp = _host_i32(host_prefix_lens, batch, "host_prefix_lens")
+    hw = _host_i32(host_window_lens, batch, "host_window_lens")
     if max_prefix_len is None:
-        max_prefix_len = int(prefix_lens.max().item()) if batch else 0
+        max_prefix_len = int(hp.max()) if batch else 0
     if max_window_len is None:
-        max_window_len = int(window_lens.max().item()) if batch else 0
+        max_window_len = int(hw.max()) if batch else 0
     stream = _stream(q.device)
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(max_window_len), MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode),
-                    float(softmax_scale or 0.0), int(kv_split_tokens), None, 0, stream)
+                    float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), _ptr(hw), None, 0, stream)
     need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
     if need == ctypes.c_size_t(-1).value:
         _check("mbe_window_attention", lib.mbe_window_attention(
             None, ctypes.byref(kv), None, None, None, int(block_size), None, ctypes.byref(opts)))
-    ws = _workspace("attn", q.device, need, stream)
+    ws = _workspace("attn", q.device, need)
     opts.workspace = _ptr(ws)
     opts.workspace_bytes = need
     _check("mbe_window_attention", lib.mbe_window_attention(
@@ -193,21 +209,26 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
 
 
 def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size, *,
-                              out=None, softmax_scale=None, max_prefix_len=None, kv_split_tokens=0):
+                              out=None, softmax_scale=None, max_prefix_len=None, kv_split_tokens=0,
+                              host_prefix_lens=None):
     """Standard single-block step (paper, Sec. "Block diffusion"): q holds
     block_size rows per sequence."""
     lib = load()
     kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
     batch = prefix_lens.shape[0]
+    if max_prefix_len is None and host_prefix_lens is None:
+        host_prefix_lens = prefix_lens.cpu()
+    hp = _host_i32(host_prefix_lens, batch, "host_prefix_lens")
     if max_prefix_len is None:
-        max_prefix_len = int(prefix_lens.max().item()) if batch else 0
+        max_prefix_len = int(hp.max()) if batch else 0
     stream = _stream(q.device)
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
-                    int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), None, 0, stream)
+                    int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), None,
+                    None, 0, stream)
     need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
     if need == ctypes.c_size_t(-1).value:
         need = 0
-    ws = _workspace("attn", q.device, need, stream)
+    ws = _workspace("attn", q.device, need)
     opts.workspace = _ptr(ws)
     opts.workspace_bytes = need
     _check("block_diffusion_attention", lib.block_diffusion_attention(
@@ -238,7 +259,7 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
         new, conf, changed = out
     stream = _stream(dev)
     need = lib.mbe_edit_select_workspace_size(rows, v)
-    ws = _workspace("edit", dev, need if need != ctypes.c_size_t(-1).value else 0, stream)
+    ws = _workspace("edit", dev, need if need != ctypes.c_size_t(-1).value else 0)
     _check("mbe_edit_select", lib.mbe_edit_select(
         _ptr(logits), rows, v, ld, _ptr(cur_tokens), ctypes.c_float(threshold), _ptr(new), _ptr(conf),
         _ptr(changed), _ptr(ws), need if ws is not None else 0, stream))

@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -41,15 +42,22 @@ bool debug_checks() {
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Split-KV plan for the attention calls, from host-known bounds only.
+// Split-KV plan for the attention calls, from host-known values only.
 struct AttnPlan {
   int32_t group = 0, qtiles = 0, splits = 1, kv_chunk = 0;
-  int64_t units = 0, units_per_xcd = 0;
-  size_t counters_off = 0, part_o_off = 0, part_ml_off = 0, bytes = 0;
+  int64_t groups = 0, slots_per_xcd = 0;
+  size_t part_o_off = 0, part_ml_off = 0, bytes = 0;
+  int32_t order_n = 0;
+  uint16_t order[mbe::kMaxOrderedSeqs];
 };
 
+// Work units the chip runs at once: 256 CUs, one 256-row workgroup each.
+constexpr int64_t kConcurrentUnits = 256;
+constexpr int64_t kMinChunk = 256;      // shortest split, in keys
+
 mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_t block_size,
-                          int32_t window_bound, AttnPlan *pl) {
+                          int32_t window_bound, int32_t fixed_window, AttnPlan *pl) {
+  auto fixed_window_of = [fixed_window](const mbe_attn_opts *, int32_t) { return fixed_window; };
   if (!kv) return fail(MBE_ERR_NULL_ARG, "paged_kv is NULL");
   if (!o) return fail(MBE_ERR_NULL_ARG, "opts is NULL");
   if (kv->page_size != mbe::kPageSize)
@@ -85,35 +93,56 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   pl->qtiles = static_cast<int32_t>(std::max<int64_t>(1, (rows + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile));
   const int64_t base_units = static_cast<int64_t>(o->batch) * kv->num_kv_heads * pl->qtiles;
 
+  // Host copies of the lengths, when given, refine the plan.
+  const bool host = o->host_prefix_lens && (fixed_window_of(o, window_bound) >= 0 || o->host_window_lens) &&
+                    o->batch > 0 && o->batch <= mbe::kMaxOrderedSeqs;
+  std::vector<int64_t> n_seq;
+  int64_t work = 0;    // sum over work units (sequence, KV head, query tile) of the keys they read
+  if (host) {
+    n_seq.resize(o->batch);
+    for (int b = 0; b < o->batch; ++b) {
+      const int64_t P = o->host_prefix_lens[b];
+      const int64_t W = fixed_window_of(o, window_bound) >= 0 ? fixed_window_of(o, window_bound) : o->host_window_lens[b];
+      if (P < 0 || P > o->max_prefix_len || W < 0 || W > window_bound)
+        return fail(MBE_ERR_BAD_SHAPE, "host lengths of sequence %d (%lld, %lld) exceed the bounds", b,
+                    static_cast<long long>(P), static_cast<long long>(W));
+      n_seq[b] = W > 0 ? P + W : 0;
+      const int64_t qt = (pl->group * W + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile;
+      work += kv->num_kv_heads * qt * n_seq[b];
+    }
+  } else {
+    work = base_units * max_kv;
+  }
+
   int64_t chunk = o->kv_split_tokens;
-  if (chunk == 0 && base_units > mbe::kMaxCounters) {
-    chunk = std::max<int64_t>(max_kv, 1);   // enough work units without splitting
-  } else if (chunk == 0) {
-    // Aim for about 4 workgroups per CU over 256 CUs, but keep splits at
-    // least 1024 keys long so that partial results stay a small fraction of
-    // the K/V traffic.
-    const int64_t target_units = 1024;
-    int64_t splits = base_units > 0 ? (target_units + base_units - 1) / base_units : 1;
-    const int64_t max_splits = std::max<int64_t>(1, max_kv / 1024);
-    splits = std::min(std::max<int64_t>(splits, 1), max_splits);
-    chunk = (max_kv + splits - 1) / splits;
+  if (chunk == 0) {
+    // Keys per split so that the work fills the CUs once: long sequences of a
+    // small batch are split, a large batch is not (each split costs a
+    // pipeline fill and a merge of partial results).
+    chunk = std::max<int64_t>(kMinChunk, (work + kConcurrentUnits - 1) / kConcurrentUnits);
   }
   chunk = std::max<int64_t>(mbe::kKeyTile, (chunk + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
-  pl->kv_chunk = static_cast<int32_t>(chunk);
+  pl->kv_chunk = static_cast<int32_t>(std::min<int64_t>(chunk, 1LL << 30));
   pl->splits = static_cast<int32_t>(std::max<int64_t>(1, (max_kv + chunk - 1) / chunk));
-  pl->units = base_units * pl->splits;
-  pl->units_per_xcd = (pl->units + mbe::kXcds - 1) / mbe::kXcds;
-  if (pl->units_per_xcd * mbe::kXcds > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "grid too large");
+  pl->groups = static_cast<int64_t>(o->batch) * kv->num_kv_heads * pl->splits;
+  pl->slots_per_xcd = (pl->groups + mbe::kXcds - 1) / mbe::kXcds * pl->qtiles;
+  if (pl->slots_per_xcd * mbe::kXcds > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "grid too large");
+
+  // Longest sequences first (stable), so the short ones fill in at the end.
+  pl->order_n = 0;
+  if (host) {
+    std::vector<int32_t> idx(o->batch);
+    for (int b = 0; b < o->batch; ++b) idx[b] = b;
+    std::stable_sort(idx.begin(), idx.end(), [&](int32_t x, int32_t y) { return n_seq[x] > n_seq[y]; });
+    for (int b = 0; b < o->batch; ++b) pl->order[b] = static_cast<uint16_t>(idx[b]);
+    pl->order_n = o->batch;
+  }
 
   pl->bytes = 0;
   if (pl->splits > 1) {
-    if (base_units > mbe::kMaxCounters)
-      return fail(MBE_ERR_UNSUPPORTED, "split-KV over %lld query tiles exceeds %lld; use kv_split_tokens = 0",
-                  static_cast<long long>(base_units), static_cast<long long>(mbe::kMaxCounters));
     const size_t rows_all = static_cast<size_t>(pl->splits) * o->total_q * o->num_q_heads;
-    pl->counters_off = 0;
-    pl->part_o_off = mbe::kCounterBytes;
-    pl->part_ml_off = pl->part_o_off + align_up(rows_all * kv->head_dim * sizeof(float));
+    pl->part_o_off = 0;
+    pl->part_ml_off = align_up(rows_all * kv->head_dim * sizeof(float));
     pl->bytes = pl->part_ml_off + align_up(rows_all * 2 * sizeof(float));
   }
   return MBE_OK;
@@ -159,7 +188,7 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
                          int32_t fixed_window, void *out, const mbe_attn_opts *o) {
   const int32_t window_bound = fixed_window >= 0 ? fixed_window : (o ? o->max_window_len : 0);
   AttnPlan pl;
-  mbe_status st = plan_attention(kv, o, block_size, window_bound, &pl);
+  mbe_status st = plan_attention(kv, o, block_size, window_bound, fixed_window, &pl);
   if (st != MBE_OK) return st;
   if (fixed_window >= 0 && o->total_q != static_cast<int64_t>(o->batch) * fixed_window)
     return fail(MBE_ERR_BAD_SHAPE, "total_q %d != batch %d * block_size %d", o->total_q, o->batch,
@@ -192,7 +221,6 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   p.window_lens = window_lens;
   p.out = static_cast<uint16_t *>(out);
   char *ws = static_cast<char *>(o->workspace);
-  p.counters = pl.bytes ? reinterpret_cast<uint32_t *>(ws + pl.counters_off) : nullptr;
   p.part_o = pl.bytes ? reinterpret_cast<float *>(ws + pl.part_o_off) : nullptr;
   p.part_ml = pl.bytes ? reinterpret_cast<float *>(ws + pl.part_ml_off) : nullptr;
   p.batch = o->batch;
@@ -209,8 +237,10 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   p.qtiles = pl.qtiles;
   p.splits = pl.splits;
   p.kv_chunk = pl.kv_chunk;
-  p.units = pl.units;
-  p.units_per_xcd = pl.units_per_xcd;
+  p.groups = pl.groups;
+  p.slots_per_xcd = pl.slots_per_xcd;
+  p.seq_order_n = pl.order_n;
+  for (int i = 0; i < pl.order_n; ++i) p.seq_order[i] = pl.order[i];
   const float scale = o->softmax_scale > 0.f ? o->softmax_scale : 1.0f / std::sqrt(static_cast<float>(kv->head_dim));
   p.scale_log2 = scale * 1.4426950408889634f;
   const int mode = fixed_window >= 0 ? MBE_MASK_WINDOW_BIDIR : o->mask_mode;
@@ -240,7 +270,7 @@ size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const m
                                            int32_t block_size) {
   AttnPlan pl;
   if (!opts) return static_cast<size_t>(-1);
-  if (plan_attention(paged_kv, opts, block_size, opts->max_window_len, &pl) != MBE_OK)
+  if (plan_attention(paged_kv, opts, block_size, opts->max_window_len, -1, &pl) != MBE_OK)
     return static_cast<size_t>(-1);
   return pl.bytes;
 }
@@ -252,7 +282,7 @@ size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab) {
   int64_t len;
   mbe::edit_select_plan(rows, vocab, &chunks, &len);
   if (chunks <= 1) return 0;
-  return mbe::kCounterBytes + align_up(static_cast<size_t>(rows) * chunks * sizeof(mbe::EsPartial));
+  return align_up(static_cast<size_t>(rows) * chunks * sizeof(mbe::EsPartial));
 }
 
 mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
@@ -295,22 +325,11 @@ mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int6
   p.changed = changed_mask;
   if (need > 0) {
     char *ws = static_cast<char *>(workspace);
-    p.counters = reinterpret_cast<uint32_t *>(ws);
-    p.partials = reinterpret_cast<mbe::EsPartial *>(ws + mbe::kCounterBytes);
+    p.partials = reinterpret_cast<mbe::EsPartial *>(ws);
   }
   const bool vec = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && (row_stride % 8 == 0);
   hipError_t e = mbe::launch_edit_select(p, vec, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "edit select launch");
-  return MBE_OK;
-}
-
-mbe_status mbe_workspace_zero(void *workspace, size_t bytes, void *stream) {
-  if (bytes == 0) return MBE_OK;
-  if (!workspace) return fail(MBE_ERR_NULL_ARG, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
-    return fail(MBE_ERR_WORKSPACE, "workspace must be 16-byte aligned");
-  hipError_t e = mbe::launch_zero_fill(workspace, bytes, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "workspace zero fill");
   return MBE_OK;
 }
 

@@ -35,10 +35,9 @@
 // makes a max-only run over its keys and then a full run with the true
 // maximum as reference, where no exponential exceeds 1.
 //
-// Split-KV: long prefixes are cut into kv_chunk-key splits.  Each split
-// writes unnormalised O, its reference and its sum; the last split of a
-// query tile to finish (atomic arrival counter, reset after use) merges them
-// in split order: M = max m_s, O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s.
+// Split-KV: when the work would not fill the chip, long key ranges are cut
+// into kv_chunk-key splits.  Each split writes unnormalised O, its reference
+// and its sum; a second, small kernel merges them in split order.
 //
 // K/V tiles of 64 keys (four 16-token pages gathered through the page table)
 // go from HBM straight into LDS (global_load_lds_dwordx4, no registers),
@@ -183,18 +182,22 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   __shared__ __align__(1024) char lds1[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds2[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds3[Tile<D>::kBufBytes];
-  __shared__ uint32_t sh_last;
 
-  // ---- work unit: XCD-contiguous ranges of (bg, split, qtile) with qtile fastest
+  // ---- work unit.  Groups (sequence rank, KV head, split) are dealt to the
+  // XCDs round-robin in dispatch order (workgroup id % 8 is the XCD), and the
+  // qtiles query tiles of a group, which read the same keys, take consecutive
+  // slots of the same XCD so that the second finds the keys in that XCD's L2.
   const int64_t id = blockIdx.x;
-  const int64_t w = (id % kXcds) * p.units_per_xcd + id / kXcds;
-  if (w >= p.units) return;
-  const int qtile = static_cast<int>(w % p.qtiles);
-  const int64_t t1 = w / p.qtiles;
-  const int split = static_cast<int>(t1 % p.splits);
-  const int bg = static_cast<int>(t1 / p.splits);
-  const int b = bg / p.num_kv_heads;
-  const int g = bg % p.num_kv_heads;
+  const int64_t slot = id / kXcds;
+  const int64_t grp = (slot / p.qtiles) * kXcds + id % kXcds;
+  if (grp >= p.groups) return;
+  const int qtile = static_cast<int>(slot % p.qtiles);
+  const int split = static_cast<int>(grp % p.splits);
+  const int64_t rg = grp / p.splits;
+  const int rank = static_cast<int>(rg / p.num_kv_heads);
+  const int g = static_cast<int>(rg % p.num_kv_heads);
+  const int b = rank < p.seq_order_n ? p.seq_order[rank] : rank;
+  const int bg = b * p.num_kv_heads + g;
 
   const int G = p.group;
   // lengths are clamped to the host-validated bounds, so a wrong device value
@@ -517,7 +520,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     return;
   }
 
-  // split-KV: write this split's partial result
+  // split-KV: write this split's partial result (merged by the merge kernel)
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
@@ -538,53 +541,68 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       *reinterpret_cast<float2 *>(pml) = make_float2(m_ref[qb], l_tot[qb]);
     }
   }
-  __threadfence();
-  __syncthreads();
-  const int64_t group = (static_cast<int64_t>(bg)) * p.qtiles + qtile;
-  if (tid == 0) sh_last = atomicAdd(&p.counters[group], 1u);
-  __syncthreads();
-  if (sh_last != static_cast<uint32_t>(nsplit - 1)) return;
-  __threadfence();
+}
 
-  // last split of this query tile: merge all splits in split order
-  const int rows_here = min(kRowsPerTile, M - row0);
+// Split-KV merge, run after the main kernel when some sequence was split (the
+// kernel boundary makes every partial result visible; no cross-workgroup
+// fences inside the main kernel).  Block (x, b) merges items x*256 .. of
+// sequence b, an item being 4 dims of one (window row, query head):
+//   M = max m_s,  O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s   (split order).
+template <int D>
+__global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams p) {
+  const int b = blockIdx.y;
+  const int P = min(max(p.prefix_lens[b], 0), p.max_prefix);
+  const int W = p.fixed_window >= 0 ? p.fixed_window : min(max(p.window_lens[b], 0), p.max_window);
+  const int n_all = P + W;
+  const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
+  if (nsplit == 1) return;                  // written directly by the main kernel
   constexpr int D4 = D / 4;
-  for (int item = tid; item < rows_here * D4; item += kT) {
-    const int rr = row0 + item / D4;
-    const int d0 = (item % D4) * 4;
-    const int i = rr / G;
-    if (cu + i >= p.total_q) continue;
-    const int hq = g * G + rr % G;
-    const int64_t rowidx = static_cast<int64_t>(cu + i) * p.num_q_heads + hq;
-    float mmax = kNegInf;
-    for (int sp = 0; sp < nsplit; ++sp) mmax = fmaxf(mmax, p.part_ml[(sp * split_stride + rowidx) * 2]);
-    float lsum = 0.f;
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float2 ml = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
-      if (ml.x == kNegInf) continue;          // split saw no key of this row
-      const float wgt = __builtin_amdgcn_exp2f(ml.x - mmax);
-      lsum += wgt * ml.y;
-      const float4 po = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
-      o.x += wgt * po.x;
-      o.y += wgt * po.y;
-      o.z += wgt * po.z;
-      o.w += wgt * po.w;
-    }
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    uint2 st;
-    st.x = pack_bf16x2(o.x * inv, o.y * inv);
-    st.y = pack_bf16x2(o.z * inv, o.w * inv);
-    *reinterpret_cast<uint2 *>(p.out + rowidx * D + d0) = st;
+  const int64_t items = static_cast<int64_t>(W) * p.num_q_heads * D4;
+  const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (item >= items) return;
+  int cu = 0;
+  if (p.fixed_window >= 0) {
+    cu = b * p.fixed_window;
+  } else {
+    for (int j = 0; j < b; ++j) cu += min(max(p.window_lens[j], 0), p.max_window);
   }
-  if (tid == 0) p.counters[group] = 0u;    // ready for the next call
+  const int64_t r = item / D4;              // (window row, query head) within the sequence
+  const int d0 = static_cast<int>(item % D4) * 4;
+  if (cu + r / p.num_q_heads >= p.total_q) return;
+  const int64_t rowidx = static_cast<int64_t>(cu) * p.num_q_heads + r;
+  const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
+  float mmax = kNegInf;
+  for (int sp = 0; sp < nsplit; ++sp) mmax = fmaxf(mmax, p.part_ml[(sp * split_stride + rowidx) * 2]);
+  float lsum = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const float2 ml = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
+    if (ml.x == kNegInf) continue;          // split saw no key of this row
+    const float wgt = __builtin_amdgcn_exp2f(ml.x - mmax);
+    lsum += wgt * ml.y;
+    const float4 po = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
+    o.x += wgt * po.x;
+    o.y += wgt * po.y;
+    o.z += wgt * po.z;
+    o.w += wgt * po.w;
+  }
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  uint2 st;
+  st.x = pack_bf16x2(o.x * inv, o.y * inv);
+  st.y = pack_bf16x2(o.z * inv, o.w * inv);
+  *reinterpret_cast<uint2 *>(p.out + rowidx * D + d0) = st;
 }
 
 template <int D, int MODE>
 hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
-  const int64_t grid = p.units_per_xcd * kXcds;
+  const int64_t grid = p.slots_per_xcd * kXcds;
   hipLaunchKernelGGL((window_attention_kernel<D, MODE>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
                      stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.splits == 1) return e;
+  const int64_t items = static_cast<int64_t>(p.max_window) * p.num_q_heads * (D / 4);
+  const dim3 mgrid(static_cast<unsigned>((items + 255) / 256), static_cast<unsigned>(p.batch));
+  hipLaunchKernelGGL((window_attention_merge_kernel<D>), mgrid, dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 

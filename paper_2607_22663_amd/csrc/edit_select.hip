@@ -17,9 +17,9 @@
 // the end to find the index (64 bytes per thread, from cache), which keeps
 // the argmax bookkeeping out of the per-element loop.
 // Threads then merge (max, lowest index among equals, rescaled sum) in a
-// fixed tree; rows split over several workgroups write partials, and the
-// last workgroup of the row (atomic arrival counter, reset after use) merges
-// them in chunk order, so results are bitwise reproducible.
+// fixed tree.  Rows split over several workgroups (few rows) write partials
+// that a small finalize kernel merges in chunk order, so results are bitwise
+// reproducible.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -71,6 +71,16 @@ __device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int
 #pragma unroll
     for (int k = 0; k < 8; ++k) x[k] = (e0 + k < end) ? bf16_at(row + e0 + k) : -INFINITY;
   }
+}
+
+// The token-to-token decision for one row from its (max, argmax, sum).
+__device__ __forceinline__ void decide(const EsParams &p, int64_t row, float m, float s, int32_t idx) {
+  const int32_t cur = p.cur[row];
+  const float conf = 1.0f / s;          // correctly rounded division
+  const bool change = (m != -INFINITY) && (idx != cur) && (conf >= p.threshold);
+  p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
+  p.new_tokens[row] = change ? idx : cur;
+  p.changed[row] = change ? 1 : 0;
 }
 
 template <bool VEC>
@@ -162,38 +172,23 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   idx = sh_i[0];
   for (int w = 1; w < kT / 64; ++w) merge(m, s, idx, sh_m[w], sh_s[w], sh_i[w]);
 
-  if (p.chunks > 1) {
+  if (p.chunks > 1) {     // merged by the finalize kernel
     p.partials[row * p.chunks + chunk] = EsPartial{m, s, idx, 0};
-    __threadfence();
-    const uint32_t arrived = atomicAdd(&p.counters[row], 1u);
-    if (arrived != static_cast<uint32_t>(p.chunks - 1)) return;
-    __threadfence();
-    const EsPartial *pp = p.partials + row * p.chunks;
-    EsPartial first = pp[0];
-    m = first.m;
-    s = first.s;
-    idx = first.idx;
-    for (int c = 1; c < p.chunks; ++c) {
-      const EsPartial q = pp[c];
-      merge(m, s, idx, q.m, q.s, q.idx);
-    }
-    p.counters[row] = 0u;     // ready for the next call
+    return;
   }
-
-  const int32_t cur = p.cur[row];
-  const float conf = 1.0f / s;          // correctly rounded division
-  const bool change = (m != -INFINITY) && (idx != cur) && (conf >= p.threshold);
-  p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
-  p.new_tokens[row] = change ? idx : cur;
-  p.changed[row] = change ? 1 : 0;
+  decide(p, row, m, s, idx);
 }
 
-__global__ void zero_fill_kernel(uint4 *p, size_t n16, uint8_t *tail, size_t ntail) {
-  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
-  for (size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n16; i += stride)
-    p[i] = make_uint4(0, 0, 0, 0);
-  if (blockIdx.x == 0)
-    for (size_t i = threadIdx.x; i < ntail; i += blockDim.x) tail[i] = 0;
+// Rows reduced in several chunks: one thread per row merges the chunk
+// partials in chunk order (the kernel boundary makes them visible).
+__global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (row >= p.rows) return;
+  const EsPartial *pp = p.partials + row * p.chunks;
+  float m = pp[0].m, s = pp[0].s;
+  int32_t idx = pp[0].idx;
+  for (int c = 1; c < p.chunks; ++c) merge(m, s, idx, pp[c].m, pp[c].s, pp[c].idx);
+  decide(p, row, m, s, idx);
 }
 
 }  // namespace
@@ -203,7 +198,7 @@ void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chu
   // least 4096 elements so each thread still streams two full iterations.
   const int64_t target_wgs = 2048;
   int64_t c = 1;
-  if (rows < target_wgs && rows <= kMaxCounters) {
+  if (rows < target_wgs) {
     c = (target_wgs + rows - 1) / rows;
     const int64_t max_c = (vocab + 4095) / 4096;
     if (c > max_c) c = max_c;
@@ -224,17 +219,10 @@ hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t 
     hipLaunchKernelGGL(edit_select_kernel<true>, grid, dim3(kT), 0, stream, p);
   else
     hipLaunchKernelGGL(edit_select_kernel<false>, grid, dim3(kT), 0, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_zero_fill(void *ptr, size_t bytes, hipStream_t stream) {
-  const size_t n16 = bytes / 16;
-  const size_t ntail = bytes - n16 * 16;
-  size_t blocks = (n16 + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(zero_fill_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
-                     reinterpret_cast<uint4 *>(ptr), n16, static_cast<uint8_t *>(ptr) + n16 * 16, ntail);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.chunks == 1) return e;
+  hipLaunchKernelGGL(edit_select_finalize_kernel, dim3(static_cast<unsigned>((p.rows + 255) / 256)), dim3(256), 0,
+                     stream, p);
   return hipGetLastError();
 }
 

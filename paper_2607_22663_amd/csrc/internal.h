@@ -15,13 +15,9 @@ constexpr int kRowsPerWave = 64;      // packed (window position, q head) rows p
 constexpr int kWaves = 4;
 constexpr int kRowsPerTile = kRowsPerWave * kWaves;   // rows per workgroup
 constexpr int kXcds = 8;              // MI355X: workgroups go round-robin over 8 XCDs
+constexpr int kMaxOrderedSeqs = 1024; // dispatch order passed in the kernel arguments
 
-// Every workspace starts with a fixed region of arrival counters.  It is
-// zero-filled once and every call leaves the counters it used at zero; no
-// call ever writes partial results into it, whatever the shapes, so a
-// workspace can be reused across calls of different shapes.
-constexpr size_t kCounterBytes = 65536;
-constexpr int64_t kMaxCounters = kCounterBytes / sizeof(uint32_t);
+
 
 struct AttnParams {
   const uint16_t *q;          // bf16 [total_q][Hq][D]
@@ -33,13 +29,17 @@ struct AttnParams {
   uint16_t *out;              // bf16 [total_q][Hq][D]
   float *part_o;              // fp32 [splits][total_q][Hq][D]   (split-KV only)
   float *part_ml;             // fp32 [splits][total_q][Hq][2]   (split-KV only)
-  uint32_t *counters;         // [batch][Hkv][qtiles]            (split-KV only)
   int32_t batch, num_q_heads, num_kv_heads, group, num_pages, max_pages;
   int32_t block_size, total_q, fixed_window;
   int32_t max_prefix, max_window;   // host-validated bounds; device lengths are clamped to them
   int32_t qtiles, splits, kv_chunk;
-  int64_t units, units_per_xcd;
+  int64_t groups;             // (sequence rank, KV head, split) groups of qtiles work units
+  int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
+  // Sequences in the order their work is dispatched (longest first), when the
+  // host knows the lengths; seq_order_n == 0 means natural order.
+  int32_t seq_order_n;
+  uint16_t seq_order[kMaxOrderedSeqs];
 };
 
 hipError_t launch_window_attention(const AttnParams &p, int head_dim, int mask_mode,
@@ -67,12 +67,10 @@ struct EsParams {
   float *conf;
   uint8_t *changed;
   EsPartial *partials;      // [rows][chunks]   (chunks > 1 only)
-  uint32_t *counters;       // [rows]           (chunks > 1 only)
 };
 
 void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len);
 hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream);
 
-hipError_t launch_zero_fill(void *ptr, size_t bytes, hipStream_t stream);
 
 }  // namespace mbe

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert len(names) == 8, names
+    assert len(names) == 7, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(mbe.EXPORTS)
@@ -40,7 +40,7 @@ def _kv(head_dim=128, page=16, hkv=4, pages=10):
 def _opts(**kw):
     base = dict(batch=1, num_q_heads=16, max_pages_per_seq=10, total_q=64, max_prefix_len=64,
                 max_window_len=64, mask_mode=0, softmax_scale=0.0, kv_split_tokens=0,
-                workspace=None, workspace_bytes=0, stream=None)
+                host_prefix_lens=None, host_window_lens=None, workspace=None, workspace_bytes=0, stream=None)
     base.update(kw)
     return mbe.AttnOpts(**base)
 

@@ -135,6 +135,24 @@ def test_workspace_reuse_across_shapes(gpu):
             assert_attn_close(out[rows], ref, f"k={k} split={split} seq {b}")
 
 
+@pytest.mark.parametrize("host", [True, False])
+def test_host_lengths_or_bounds_only(gpu, host):
+    """With host copies of the lengths the library sizes splits from the work
+    and dispatches the longest sequences first; with bounds only it uses the
+    natural order.  Both must give the oracle's result."""
+    spec = synth.AttnSpec(6, 32, 2, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 31, prefix_lens=[100, 3000, 0, 1500, 64, 2900],
+                                     window_lens=[64, 32, 96, 0, 64, 32])
+    c = case.to(DEV)
+    kw = dict(host_prefix_lens=case.prefix_lens, host_window_lens=case.window_lens) if host else \
+        dict(max_prefix_len=3000, max_window_len=96)
+    for mode in ("bidir", "block_causal"):
+        out = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, 32,
+                                   mask_mode=mode, **kw)
+        torch.cuda.synchronize()
+        assert_attn_close(out.cpu(), oracle_case(case, mode), f"host={host} {mode}")
+
+
 def test_deterministic(gpu):
     case = synth.workload_attention("single_p2048_k2_gqa16x4_d128")
     a = run_case(gpu, case, "bidir", kv_split_tokens=256)
