@@ -32,7 +32,8 @@ PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 DEFAULT_WORKLOAD = "long_context_b64_p4096to32768_k4"
 METRIC = "edit-window attention TFLOP/s (bf16) + edit-select GB/s, % of MI355X peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+CALIB_COPY_BYTES = 256 << 20     # the plain device copy bench.py runs once, for counter calibration
 
 
 def attention_work(case):
@@ -62,18 +63,96 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel, workload):
-    """HBM bytes per launch from committed rocprofv3 --pmc counters, if they were
-    taken on the current kernel sources; else None."""
+def read_traffic_file():
+    """profiles/hbm_traffic.txt: one `key=value ...` line per kernel."""
+    out = {}
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+            for line in f:
+                if line.startswith("#") or "=" not in line:
+                    continue
+                kv = dict(tok.split("=", 1) for tok in line.split())
+                out[kv["kernel"]] = kv
+    except OSError:
+        pass
+    return out
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel sources and this workload; else None."""
+    e = read_traffic_file().get(kernel)
+    if not e or e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
         return None
-    e = t.get(kernel, {})
-    if e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
-        return None
-    return e.get("bytes_per_launch")
+    return {"read_bytes": int(float(e["read_bytes"])), "write_bytes": int(float(e["write_bytes"])),
+            "bytes_per_launch": int(float(e["read_bytes"]) + float(e["write_bytes"])),
+            "calibration": e.get("calibration")}
+
+
+def _counter_rows(path):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            rows.extend(csv.DictReader(fh))
+    return rows
+
+
+def summarize_pmc(fetch_dir, write_dir, workload):
+    """Writes profiles/hbm_traffic.txt from two rocprofv3 --pmc runs of this
+    script (FETCH_SIZE, then WRITE_SIZE).  Each counter is scaled by what it
+    reads for the plain device copy of CALIB_COPY_BYTES that bench.py runs
+    before timing (the copy reads and writes that many bytes)."""
+    lines = ["# HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE (KiB per dispatch),",
+             "# each scaled by the same counter's reading for a plain 256 MiB device copy.",
+             f"# workload {workload}; kernel_sha = hash of the kernel sources the counters were taken on"]
+    scale = {}
+    per_kernel = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in _counter_rows(d) if r["Counter_Name"] == counter]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        calib = max(copies)                    # the 256 MiB copy is the largest one
+        scale[counter] = CALIB_COPY_BYTES / (calib * 1024.0)
+        for r in rows:
+            name = r["Kernel_Name"]
+            for k in ("window_attention_kernel", "window_attention_merge_kernel", "edit_select_kernel",
+                      "edit_select_finalize_kernel"):
+                if k in name:
+                    per_kernel.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
+    sha = kernel_source_hash()
+    for k, v in sorted(per_kernel.items()):
+        f = sum(v.get("FETCH_SIZE", [0])) / max(1, len(v.get("FETCH_SIZE", [0])))
+        w = sum(v.get("WRITE_SIZE", [0])) / max(1, len(v.get("WRITE_SIZE", [0])))
+        kname = {"window_attention_kernel": "window_attention", "edit_select_kernel": "edit_select"}.get(k, k)
+        lines.append(f"kernel={kname} workload={workload} kernel_sha={sha} "
+                     f"fetch_kib={f:.1f} write_kib={w:.1f} "
+                     f"read_bytes={f * 1024 * scale['FETCH_SIZE']:.0f} write_bytes={w * 1024 * scale['WRITE_SIZE']:.0f} "
+                     f"calibration=fetch_x{scale['FETCH_SIZE']:.3f},write_x{scale['WRITE_SIZE']:.3f}")
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_stats(stats_dir, out_path, command):
+    """Writes a short markdown summary of a rocprofv3 --kernel-trace --stats run."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            rows.extend(csv.DictReader(fh))
+    lines = ["# rocprofv3 kernel statistics", "", "Command (run from the repository root on one MI355X):", "",
+             "```", command, "```", "",
+             "| kernel | calls | average (us) | min (us) | max (us) | share of GPU time |", "|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r.get("TotalDurationNs", 0))):
+        lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_sample, edit_sample):
@@ -128,9 +207,19 @@ def main():
     ap.add_argument("--k", type=int, default=None, help="window blocks (span sweep workload)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--attn-sample", type=int, default=4, help="sequences the CPU oracle times")
-    ap.add_argument("--edit-sample", type=int, default=512, help="edit rows the CPU oracle times")
+    ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
+    ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/hbm_traffic.txt from two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_DIR", "OUT_MD", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --stats output folder and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload)
+        return
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -172,7 +261,7 @@ def main():
 
     # A plain copy of known size, outside the timed region: its rocprofv3 counter
     # readings calibrate the HBM byte counters of the other kernels.
-    calib = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    calib = torch.empty(CALIB_COPY_BYTES, dtype=torch.uint8, device=dev)
     calib2 = torch.empty_like(calib)
     calib2.copy_(calib)
     torch.cuda.synchronize()
@@ -250,7 +339,8 @@ def main():
         "roofline": {"kernel": "window_attention_kernel<128,0>", "bound": "mfma",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic["bytes_per_launch"] if traffic else None,
+                     "traffic_detail": traffic, "algorithmic_bytes": attn_bytes},
         "wall_s": round(wall, 3),
     }
     if not args.no_cpu_baseline and edit_case is not None:

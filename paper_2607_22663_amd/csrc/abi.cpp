@@ -1,7 +1,7 @@
 // C ABI of libmbe: argument validation, split planning, workspace sizing and
 // dispatch to the HIP kernels.  Every check runs before the first HIP call,
 // so the validation paths work on a machine without a GPU.
-#include "../../include/mbe.h"
+#include "mbe.h"
 
 #include <hip/hip_runtime.h>
 
