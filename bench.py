@@ -84,9 +84,12 @@ def measured_traffic(kernel, workload):
     e = read_traffic_file().get(kernel)
     if not e or e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
         return None
-    return {"read_bytes": int(float(e["read_bytes"])), "write_bytes": int(float(e["write_bytes"])),
-            "bytes_per_launch": int(float(e["read_bytes"]) + float(e["write_bytes"])),
-            "calibration": e.get("calibration")}
+    out = {"read_bytes": int(float(e["read_bytes"])), "write_bytes": int(float(e["write_bytes"])),
+           "bytes_per_launch": int(float(e["read_bytes"]) + float(e["write_bytes"])),
+           "calibration": e.get("calibration")}
+    if "req_read_bytes" in e:
+        out["read_bytes_by_request_size"] = int(float(e["req_read_bytes"]))
+    return out
 
 
 def _counter_rows(path):
@@ -100,56 +103,115 @@ def _counter_rows(path):
     return rows
 
 
-def summarize_pmc(fetch_dir, write_dir, workload):
-    """Writes profiles/hbm_traffic.txt from two rocprofv3 --pmc runs of this
-    script (FETCH_SIZE, then WRITE_SIZE).  Each counter is scaled by what it
-    reads for the plain device copy of CALIB_COPY_BYTES that bench.py runs
-    before timing (the copy reads and writes that many bytes)."""
+_KERNELS = {"window_attention_kernel": "window_attention", "window_attention_merge_kernel": "window_attention_merge",
+            "edit_select_kernel": "edit_select", "edit_select_finalize_kernel": "edit_select_finalize"}
+
+
+def _kernel_key(name):
+    # "window_attention_kernel<" also prefixes the merge kernel's name: match on the full token
+    for k in sorted(_KERNELS, key=len, reverse=True):
+        if k + "<" in name or k + "(" in name:
+            return _KERNELS[k]
+    return None
+
+
+def summarize_pmc(dirs, workload):
+    """Writes profiles/hbm_traffic.txt from rocprofv3 --pmc runs of this script:
+    FETCH_SIZE, then WRITE_SIZE, then optionally TCC_EA0_RDREQ_{32B,64B,128B}_sum
+    plus TCC_EA0_RDREQ_sum.  FETCH_SIZE and WRITE_SIZE are each scaled by what
+    the counter reads for the plain device copy of CALIB_COPY_BYTES that
+    bench.py runs before timing (the copy reads and writes that many bytes).
+    The request-size pass counts read bytes directly (32, 64 or 128 bytes per
+    request), which the copy scaling cannot do when a kernel's mix of request
+    sizes differs from the copy's."""
+    fetch_dir, write_dir = dirs[0], dirs[1]
+    req_dir = dirs[2] if len(dirs) > 2 else None
     lines = ["# HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE (KiB per dispatch),",
-             "# each scaled by the same counter's reading for a plain 256 MiB device copy.",
+             "# each scaled by the same counter's reading for a plain 256 MiB device copy;",
+             "# req_read_bytes = 32*RDREQ_32B + 64*RDREQ_64B + 128*RDREQ_128B (TCC to memory read requests).",
              f"# workload {workload}; kernel_sha = hash of the kernel sources the counters were taken on"]
     scale = {}
     per_kernel = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = [r for r in _counter_rows(d) if r["Counter_Name"] == counter]
         copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
-        calib = max(copies)                    # the 256 MiB copy is the largest one
-        scale[counter] = CALIB_COPY_BYTES / (calib * 1024.0)
+        scale[counter] = CALIB_COPY_BYTES / (max(copies) * 1024.0)   # the 256 MiB copy is the largest
         for r in rows:
-            name = r["Kernel_Name"]
-            for k in ("window_attention_kernel", "window_attention_merge_kernel", "edit_select_kernel",
-                      "edit_select_finalize_kernel"):
-                if k in name:
-                    per_kernel.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
+            k = _kernel_key(r["Kernel_Name"])
+            if k:
+                per_kernel.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
+    if req_dir:
+        for r in _counter_rows(req_dir):
+            k = _kernel_key(r["Kernel_Name"])
+            if k:
+                per_kernel.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     sha = kernel_source_hash()
+
+    def avg(v, c):
+        x = v.get(c)
+        return sum(x) / len(x) if x else None
+
     for k, v in sorted(per_kernel.items()):
-        f = sum(v.get("FETCH_SIZE", [0])) / max(1, len(v.get("FETCH_SIZE", [0])))
-        w = sum(v.get("WRITE_SIZE", [0])) / max(1, len(v.get("WRITE_SIZE", [0])))
-        kname = {"window_attention_kernel": "window_attention", "edit_select_kernel": "edit_select"}.get(k, k)
-        lines.append(f"kernel={kname} workload={workload} kernel_sha={sha} "
-                     f"fetch_kib={f:.1f} write_kib={w:.1f} "
-                     f"read_bytes={f * 1024 * scale['FETCH_SIZE']:.0f} write_bytes={w * 1024 * scale['WRITE_SIZE']:.0f} "
-                     f"calibration=fetch_x{scale['FETCH_SIZE']:.3f},write_x{scale['WRITE_SIZE']:.3f}")
+        f, w = avg(v, "FETCH_SIZE"), avg(v, "WRITE_SIZE")
+        line = (f"kernel={k} workload={workload} kernel_sha={sha} fetch_kib={f:.1f} write_kib={w:.1f} "
+                f"read_bytes={f * 1024 * scale['FETCH_SIZE']:.0f} write_bytes={w * 1024 * scale['WRITE_SIZE']:.0f} "
+                f"calibration=fetch_x{scale['FETCH_SIZE']:.3f},write_x{scale['WRITE_SIZE']:.3f}")
+        n32, n64, n128 = (avg(v, f"TCC_EA0_RDREQ_{b}_sum") for b in ("32B", "64B", "128B"))
+        if n32 is not None and n64 is not None and n128 is not None:
+            line += (f" rdreq_32b={n32:.0f} rdreq_64b={n64:.0f} rdreq_128b={n128:.0f} "
+                     f"rdreq_all={avg(v, 'TCC_EA0_RDREQ_sum') or 0:.0f} "
+                     f"req_read_bytes={32 * n32 + 64 * n64 + 128 * n128:.0f}")
+        lines.append(line)
     with open(TRAFFIC_FILE, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
-def summarize_stats(stats_dir, out_path, command):
-    """Writes a short markdown summary of a rocprofv3 --kernel-trace --stats run."""
+def summarize_stats(stats_dir, bench_stdout, out_path, command):
+    """Writes a short markdown summary of a rocprofv3 --kernel-trace --stats run
+    of this script: rocprofv3's per-kernel statistics, the average over the
+    timed dispatches from the kernel trace, and the JSON line that the same
+    profiled run printed (its event-timed kernel durations)."""
     import csv
     import glob
-    files = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)
-    rows = []
-    for f in files:
-        with open(f) as fh:
-            rows.extend(csv.DictReader(fh))
+
+    def read(pattern):
+        rows = []
+        for f in glob.glob(os.path.join(stats_dir, "**", pattern), recursive=True):
+            with open(f) as fh:
+                rows.extend(csv.DictReader(fh))
+        return rows
+
+    stats, trace = read("*kernel_stats.csv"), read("*kernel_trace.csv")
+    line = None
+    with open(bench_stdout) as f:
+        for ln in f:
+            if ln.startswith("{"):
+                line = json.loads(ln)
     lines = ["# rocprofv3 kernel statistics", "", "Command (run from the repository root on one MI355X):", "",
              "```", command, "```", "",
              "| kernel | calls | average (us) | min (us) | max (us) | share of GPU time |", "|---|---|---|---|---|---|"]
-    for r in sorted(rows, key=lambda r: -float(r.get("TotalDurationNs", 0))):
+    for r in sorted(stats, key=lambda r: -float(r.get("TotalDurationNs", 0))):
         lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
+    if trace and line:
+        steps = int(line["steps"])
+        lines += ["", f"Average over the {steps} timed dispatches (the last {steps} of each kernel in the trace) "
+                  "next to the same run's HIP-event timing:", "",
+                  "| kernel | rocprofv3 trace average (us) | bench.py event average (us) |", "|---|---|---|"]
+        ev = {"window_attention": line["attention"]["ms"] * 1e3,
+              "edit_select": (line.get("edit_select") or {}).get("ms", 0) * 1e3}
+        by = {}
+        for r in sorted(trace, key=lambda r: int(r["Start_Timestamp"])):
+            k = _kernel_key(r["Kernel_Name"])
+            if k:
+                by.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        for k, d in sorted(by.items()):
+            d = d[-steps:]
+            lines.append(f"| {k} | {sum(d) / len(d):.2f} | {ev[k]:.2f} |" if k in ev else
+                         f"| {k} | {sum(d) / len(d):.2f} | (inside the attention call) |")
+    if line:
+        lines += ["", "JSON line printed by the profiled run:", "", "```", json.dumps(line), "```"]
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -209,13 +271,14 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
-    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="write profiles/hbm_traffic.txt from two rocprofv3 --pmc output folders and exit")
-    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_DIR", "OUT_MD", "COMMAND"),
-                    help="write a markdown summary of a rocprofv3 --stats output folder and exit")
+    ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
+                    help="write profiles/hbm_traffic.txt from rocprofv3 --pmc output folders (FETCH_SIZE, "
+                         "WRITE_SIZE, optionally the TCC_EA0_RDREQ_* request-size pass) and exit")
+    ap.add_argument("--summarize-stats", nargs=4, metavar=("STATS_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --kernel-trace --stats run and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload)
+        summarize_pmc(args.summarize_pmc, args.workload)
         return
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
@@ -335,7 +398,9 @@ def main():
                       "gflop": round(flops / 1e9, 2), "algorithmic_mb": round(attn_bytes / 1e6, 1)},
         "edit_select": ({"ms": round(t_edit * 1e3, 4), "gbs": round(edit_gbs, 1),
                          "pct_hbm_peak": round(100 * edit_gbs / PEAK_HBM_GBS, 2),
-                         "algorithmic_mb": round(e_bytes / 1e6, 1)} if edit_case is not None else None),
+                         "algorithmic_mb": round(e_bytes / 1e6, 1),
+                         "traffic": measured_traffic("edit_select", args.workload)}
+                        if edit_case is not None else None),
         "roofline": {"kernel": "window_attention_kernel<128,0>", "bound": "mfma",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),

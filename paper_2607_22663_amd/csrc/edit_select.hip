@@ -8,18 +8,18 @@
 // Decoding").  Ties go to the lowest index; the test is conf >= threshold.
 //
 // One HBM pass per row.  Each workgroup (256 threads) reduces one chunk of a
-// row; each thread streams 16-byte bf16 vectors, 4 in flight, and keeps
+// row; each thread streams 16-byte bf16 vectors, 2 in flight, and keeps
 //   m       its running maximum,
 //   s       sum of exp(x - m), rescaled when m grows,
 //   it_max  the iteration where m was first reached.
 // Elements of one thread are visited in increasing index order, so its first
-// occurrence of m lies in iteration it_max; that iteration is re-read once at
-// the end to find the index (64 bytes per thread, from cache), which keeps
-// the argmax bookkeeping out of the per-element loop.
-// Threads then merge (max, lowest index among equals, rescaled sum) in a
-// fixed tree.  Rows split over several workgroups (few rows) write partials
-// that a small finalize kernel merges in chunk order, so results are bitwise
-// reproducible.
+// occurrence of m lies in iteration it_max.  Threads merge (max, rescaled
+// sum) in a fixed tree; then only the threads whose own maximum equals the
+// chunk maximum re-read their iteration it_max to find its first index, and a
+// min over the workgroup picks the lowest.  This keeps the argmax bookkeeping
+// out of the per-element loop at the cost of a few cache lines per chunk.
+// Rows split over several workgroups (few rows) write partials that a small
+// finalize kernel merges in chunk order, so results are bitwise reproducible.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -27,6 +27,8 @@
 
 namespace mbe {
 namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kU = kEsVecPerThread;
@@ -41,19 +43,21 @@ __device__ __forceinline__ float bf16_at(const uint16_t *p) {
 // exp(d) for d <= 0 through the hardware base-2 exponential.
 __device__ __forceinline__ float exp_neg(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
 
-// Merge partial (m, s, i) with (m2, s2, i2): larger max wins, equal maxima keep
-// the lower index, sums are rescaled to the common max.
-__device__ __forceinline__ void merge(float &m, float &s, int32_t &i, float m2, float s2, int32_t i2) {
+// Merge partial (m, s) with (m2, s2): the sums are rescaled to the common max.
+__device__ __forceinline__ void merge_ms(float &m, float &s, float m2, float s2) {
   const float M = fmaxf(m, m2);
-  if (M == -INFINITY) {       // both empty so far
-    i = min(i, i2);
-    return;
-  }
+  if (M == -INFINITY) return;     // both empty so far
   const float a = (m == -INFINITY) ? 0.f : s * exp_neg(m - M);
   const float b = (m2 == -INFINITY) ? 0.f : s2 * exp_neg(m2 - M);
   s = a + b;
-  i = (m > m2) ? i : ((m2 > m) ? i2 : min(i, i2));
   m = M;
+}
+
+// Merge partial (m, s, i) with (m2, s2, i2): larger max wins, equal maxima keep
+// the lower index.
+__device__ __forceinline__ void merge(float &m, float &s, int32_t &i, float m2, float s2, int32_t i2) {
+  i = (m > m2) ? i : ((m2 > m) ? i2 : min(i, i2));
+  merge_ms(m, s, m2, s2);
 }
 
 // Loads vector unit `unit` (elements 8*unit .. 8*unit+7) as 8 floats; elements
@@ -62,11 +66,13 @@ template <bool VEC>
 __device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int64_t end, float x[8]) {
   const int64_t e0 = unit * 8;
   if (VEC && e0 + 8 <= end) {
-    const uint4 w = *reinterpret_cast<const uint4 *>(row + e0);
-    x[0] = bf16_lo(w.x); x[1] = bf16_hi(w.x);
-    x[2] = bf16_lo(w.y); x[3] = bf16_hi(w.y);
-    x[4] = bf16_lo(w.z); x[5] = bf16_hi(w.z);
-    x[6] = bf16_lo(w.w); x[7] = bf16_hi(w.w);
+    // Streaming load: each logit is read once, so it is not kept in cache.
+    const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + e0));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[2 * k] = bf16_lo(w[k]);
+      x[2 * k + 1] = bf16_hi(w[k]);
+    }
   } else {
 #pragma unroll
     for (int k = 0; k < 8; ++k) x[k] = (e0 + k < end) ? bf16_at(row + e0 + k) : -INFINITY;
@@ -133,9 +139,32 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
     s += acc;
   }
 
-  // First index of m among this thread's elements: it lies in iteration it_max.
+  // (max, rescaled sum) over the workgroup: wave butterfly, then the four
+  // wave results in wave order.
+  const float m_own = m;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float m2 = __shfl_xor(m, o);
+    const float s2 = __shfl_xor(s, o);
+    merge_ms(m, s, m2, s2);
+  }
+  const int wave = tid / 64;
+  if ((tid & 63) == 0) {
+    sh_m[wave] = m;
+    sh_s[wave] = s;
+  }
+  __syncthreads();
+  m = sh_m[0];
+  s = sh_s[0];
+#pragma unroll
+  for (int w = 1; w < kT / 64; ++w) merge_ms(m, s, sh_m[w], sh_s[w]);
+
+  // First index of the chunk maximum.  Only threads whose own maximum equals
+  // it look: their first occurrence lies in iteration it_max, re-read once
+  // (the other threads read nothing more, so the re-read costs a few cache
+  // lines per chunk instead of one per thread).
   int32_t idx = INT32_MAX;
-  if (it_max >= 0) {
+  if (m != -INFINITY && m_own == m) {
     const int64_t base = u0 + static_cast<int64_t>(it_max) * kT * kU;
     for (int j = 0; j < kU && idx == INT32_MAX; ++j) {
       const int64_t unit = base + j * kT + tid;
@@ -150,27 +179,13 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
       }
     }
   }
-
-  // Wave reduction in a fixed butterfly order.
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float m2 = __shfl_xor(m, o);
-    const float s2 = __shfl_xor(s, o);
-    const int32_t i2 = __shfl_xor(idx, o);
-    merge(m, s, idx, m2, s2, i2);
-  }
-  const int wave = tid / 64;
-  if ((tid & 63) == 0) {
-    sh_m[wave] = m;
-    sh_s[wave] = s;
-    sh_i[wave] = idx;
-  }
+  for (int o = 32; o >= 1; o >>= 1) idx = min(idx, __shfl_xor(idx, o));
+  if ((tid & 63) == 0) sh_i[wave] = idx;
   __syncthreads();
   if (tid != 0) return;
-  m = sh_m[0];
-  s = sh_s[0];
-  idx = sh_i[0];
-  for (int w = 1; w < kT / 64; ++w) merge(m, s, idx, sh_m[w], sh_s[w], sh_i[w]);
+#pragma unroll
+  for (int w = 0; w < kT / 64; ++w) idx = min(idx, sh_i[w]);
 
   if (p.chunks > 1) {     // merged by the finalize kernel
     p.partials[row * p.chunks + chunk] = EsPartial{m, s, idx, 0};
@@ -195,7 +210,7 @@ __global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
 
 void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len) {
   // Enough workgroups to cover 256 CUs several times over; a chunk keeps at
-  // least 4096 elements so each thread still streams two full iterations.
+  // least 4096 elements, one full iteration of the workgroup.
   const int64_t target_wgs = 2048;
   int64_t c = 1;
   if (rows < target_wgs) {

@@ -47,7 +47,7 @@ hipError_t launch_window_attention(const AttnParams &p, int head_dim, int mask_m
 
 // ------------------------------------------------------------ edit selection
 constexpr int kEsThreads = 256;
-constexpr int kEsVecPerThread = 4;   // 16-byte loads per thread per iteration
+constexpr int kEsVecPerThread = 2;   // 16-byte loads per thread per iteration
 
 struct EsPartial {
   float m;        // running max logit
