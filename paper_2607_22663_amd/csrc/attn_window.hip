@@ -40,13 +40,15 @@
 // and its sum; a second, small kernel merges them in split order.
 //
 // K/V tiles of 64 keys (four 16-token pages gathered through the page table)
-// go from HBM straight into LDS (global_load_lds_dwordx4, no registers),
-// double buffered.  Each wave instruction fills 1 KB of LDS; the lanes fetch
-// their 16-byte chunks in an XOR-swizzled order, so the global reads stay
-// contiguous per page while the MFMA operand reads are free of bank
-// conflicts.  Workgroup ids are mapped so that each XCD runs a contiguous
-// range of work units and the query tiles sharing a key range run back to
-// back on the same XCD (shared L2).
+// go from HBM straight into LDS (global_load_lds_dwordx4, no registers), four
+// buffers with three tiles in flight.  Wave w fetches page w of each tile:
+// each load instruction reads 1 KB of one page (a scalar page base plus a
+// fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled and a
+// V page ([D][16 keys]) with the two 8-key halves of every other group of 8
+// dims swapped, so that the MFMA operand reads are free of bank conflicts.
+// Workgroup ids are mapped so that each XCD runs a contiguous range of work
+// units and the query tiles sharing a key range run back to back on the same
+// XCD (shared L2).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -67,14 +69,17 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kT = kWaves * 64;
 constexpr float kNegInf = -INFINITY;
 constexpr float kSumLimit = 0x1p64f;   // row sums above this trigger the exact rerun
+constexpr bf16x2 kOnes2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 
 template <int D>
 struct Tile {
   static constexpr int kRowChunks = D / 8;                   // 16-byte chunks per K row
-  static constexpr int kKBytes = kKeyTile * D * 2;           // K: 64 keys x D
-  static constexpr int kVBytes = D * kKeyTile * 2;           // V^T: D dims x 64 keys
+  static constexpr int kPageBytes = kPageSize * D * 2;       // one page of one KV head, K or V
+  static constexpr int kKBytes = kKeyTile * D * 2;           // K: 64 keys x D, row-major, swizzled
+  static constexpr int kVBytes = D * kKeyTile * 2;           // V: 4 pages of [D][16 keys]
   static constexpr int kBufBytes = kKBytes + kVBytes;
-  static constexpr int kLoads = kKeyTile * D / 8 / kT;       // direct loads per thread per tile (K and V each)
+  static constexpr int kLoads = kPageBytes / 1024;           // 1 KB direct loads per page (per wave, K and V each)
+  static_assert(kLoads * kWaves * 1024 == kKBytes, "one page per wave");
 };
 
 // LDS chunk position of global chunk j of K row r (XOR swizzle; an involution).
@@ -82,9 +87,10 @@ template <int D>
 __device__ __forceinline__ int k_swz(int r) {
   return D == 128 ? (r & 15) : ((r >> 1) & 7);
 }
-// LDS chunk position of key chunk ci (8 keys) of V^T row d.
-__device__ __forceinline__ int v_swz(int d) { return (d >> 1) & 7; }
-
+// LDS half (16 bytes: keys 0-7 or 8-15 of a page) of half q of V dim row d.
+// The 16 lanes that LDS serves together read dims c .. c+15 of one half;
+// without the swap dims c and c+8 would share banks.
+__device__ __forceinline__ int v_half(int d, int q) { return q ^ ((d >> 3) & 1); }
 // Bit swap 2<->3 of a row index in 0..31: MFMA row -> key within a 32-key block.
 __device__ __forceinline__ int perm_row(int r) {
   return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -113,64 +119,80 @@ __device__ __forceinline__ bf16x8 lds_read8(const char *base, int byte_off) {
 
 typedef const __attribute__((address_space(4))) int32_t const_i32;
 
-// Page ids of the four pages of the 64-key tile starting at key0, read with
-// scalar loads (the page table is constant during the kernel).  Slots past
-// the table row are clamped into it and ids into the pool; such pages only
-// feed keys that are masked and whose V rows are zeroed.
-__device__ __forceinline__ void tile_pages(const AttnParams &p, int b, int key0, int (&pid)[4]) {
+// Page id of page `wv` of the 64-key tile starting at key0, read with a scalar
+// load (the page table is constant during the kernel).  Slots past the table
+// row are clamped into it and ids into the pool; such pages only feed keys
+// that are masked and whose V rows are zeroed.
+__device__ __forceinline__ int wave_page(const AttnParams &p, int b, int key0, int wv) {
   const_i32 *row = (const_i32 *)(p.page_table) + static_cast<int64_t>(b) * p.max_pages;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int slot = min(key0 / kPageSize + q, p.max_pages - 1);
-    pid[q] = min(max(row[slot], 0), p.num_pages - 1);
-  }
+  const int slot = min(key0 / kPageSize + wv, p.max_pages - 1);
+  return min(max(row[slot], 0), p.num_pages - 1);
 }
 
-// Issues the direct HBM->LDS loads of one 64-key tile (K and V) into `buf`.
+// Per-lane byte offsets, within one K page, of the chunks that the direct
+// loads j = 0 .. kLoads-1 of a wave fetch: LDS slot s = 64 (kLoads wv + j) +
+// lane of the tile holds chunk (s % RC) ^ k_swz(row) of key row s / RC, and
+// row s / RC lies in page wv.  They do not depend on the tile.
 template <int D>
-__device__ __forceinline__ void load_tile(const AttnParams &p, int g, const int (&pid)[4], char *buf) {
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6;
-  const int lane = tid & 63;
+__device__ __forceinline__ void k_load_offsets(uint32_t (&koff)[Tile<D>::kLoads]) {
   constexpr int RC = Tile<D>::kRowChunks;
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int j = 0; j < Tile<D>::kLoads; ++j) {
-    const int inst = wave * Tile<D>::kLoads + j;      // which 1 KB of the tile
-    const int s = inst * 64 + lane;                   // LDS chunk slot of this lane
-    // K: slot s holds chunk (s % RC) ^ swz of key row s / RC
-    {
-      const int row = s / RC;
-      const int chunk = (s % RC) ^ k_swz<D>(row);
-      const int64_t src = (static_cast<int64_t>(pid[row >> 4]) * p.num_kv_heads + g) * (kPageSize * D) +
-                          (row & 15) * D + chunk * 8;
-      __builtin_amdgcn_global_load_lds(p.k_pages + src, (lds_void *)(buf + inst * 1024), 16, 0, 0);
-    }
-    // V^T: slot s holds key chunk (s % 8) ^ swz of dim row s / 8
-    {
-      const int d = s >> 3;
-      const int ci = (s & 7) ^ v_swz(d);                // keys 8ci .. 8ci+7 of the tile
-      const int64_t src = (static_cast<int64_t>(pid[ci >> 1]) * p.num_kv_heads + g) * (kPageSize * D) +
-                          d * kPageSize + (ci & 1) * 8;
-      __builtin_amdgcn_global_load_lds(p.v_pages + src,
-                                       (lds_void *)(buf + Tile<D>::kKBytes + inst * 1024), 16, 0, 0);
-    }
+    const int row = (j * 64 + lane) / RC;             // key within the page
+    const int chunk = (lane % RC) ^ k_swz<D>(row);
+    koff[j] = static_cast<uint32_t>(row * (2 * D) + chunk * 16);
   }
 }
 
-// Zeroes V^T entries of keys at or past `nvalid` (tile-relative) so that
+// Issues this wave's direct HBM->LDS loads of one 64-key tile into `buf`:
+// wave wv fetches page wv of the tile, its K rows (swizzled) and its V page
+// ([D][16 keys], 8-key halves placed by v_half).  Each load reads 1 KB from
+// one page, so its address is a scalar page base plus a loop-invariant lane
+// offset (the empty asm statements keep the two apart, which selects the
+// scalar-base form of the load instead of 64-bit vector address arithmetic).
+template <int D>
+__device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, int pid,
+                                          const uint32_t (&koff)[Tile<D>::kLoads], char *buf) {
+  constexpr int PB = Tile<D>::kPageBytes;
+  pid = __builtin_amdgcn_readfirstlane(pid);   // wave-uniform; lets it live in a scalar register
+  const int64_t page = (static_cast<int64_t>(pid) * p.num_kv_heads + g) * PB;
+  uint64_t kbase = reinterpret_cast<uint64_t>(p.k_pages) + page;
+  uint64_t vbase = reinterpret_cast<uint64_t>(p.v_pages) + page;
+  asm("" : "+s"(kbase), "+s"(vbase));
+  char *kdst = buf + wv * PB;
+  char *vdst = buf + Tile<D>::kKBytes + wv * PB;
+#pragma unroll
+  for (int j = 0; j < Tile<D>::kLoads; ++j) {
+    uint32_t ko;
+    asm("" : "=v"(ko) : "0"(koff[j]), "s"(pid));
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + ko, (lds_void *)(kdst + j * 1024), 16,
+                                     0, 0);
+  }
+  // V: LDS slot j*64 + lane of the page is dim (32j + lane/2), half lane&1,
+  // and holds that dim's half v_half(d, lane & 1) (the swap is its own inverse)
+  const int lane = threadIdx.x & 63;
+  uint32_t vo;
+  asm("" : "=v"(vo) : "0"((lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4)), "s"(pid));
+#pragma unroll
+  for (int j = 0; j < Tile<D>::kLoads; ++j)
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + vo,
+                                     (lds_void *)(vdst + j * 1024), 16, 0, 0);
+}
+
+// Zeroes V entries of keys at or past `nvalid` (tile-relative) so that
 // unread page tails (which may hold anything) cannot reach the P.V product.
 template <int D>
 __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
   uint16_t *vs = reinterpret_cast<uint16_t *>(buf + Tile<D>::kKBytes);
-  for (int s = threadIdx.x; s < D * 8; s += kT) {
-    const int d = s >> 3;
-    const int ci = (s & 7) ^ v_swz(d);
-    const int k0 = ci * 8;
-    if (k0 + 8 <= nvalid) continue;
-    uint16_t *e = vs + s * 8;
+  for (int s = threadIdx.x; s < 4 * D; s += kT) {   // row s: page s / D, dim s % D, 16 keys
+    const int k0 = (s / D) * kPageSize;
+    if (k0 + kPageSize <= nvalid) continue;
+    uint16_t *e = vs + s * kPageSize;
+    const int d = s % D;
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (k0 + k >= nvalid) e[k] = 0;
+    for (int k = 0; k < kPageSize; ++k)
+      if (k0 + k >= nvalid) e[v_half(d, k >> 3) * 8 + (k & 7)] = 0;
   }
 }
 
@@ -276,13 +298,10 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   int koff[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) koff[kk] = krow * (2 * D) + (((2 * kk + h) ^ k_swz<D>(krow)) << 4);
-  // V^T: row c (+32 per dim block), key chunk 4kbk + 2mm + h
-  int voff[2][2];
-#pragma unroll
-  for (int kbk = 0; kbk < 2; ++kbk)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-      voff[kbk][mm] = Tile<D>::kKBytes + c * (kKeyTile * 2) + (((4 * kbk + 2 * mm + h) ^ v_swz(c)) << 4);
+  // V: page 2kbk + mm of the tile, dim c (+32 per dim block), keys 8h .. 8h+7
+  // of the page (dims 32db + c and c share the half swap, 32 being a
+  // multiple of 16)
+  const int voff = Tile<D>::kKBytes + c * (kPageSize * 2) + (v_half(c, h) << 4);
 
   constexpr int DB = D / 32;
   f32x16 acc_o[2][DB];
@@ -295,11 +314,21 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   if (MODE == 1) wg_min = min(ke, P + ((row0 / G) / p.block_size + 1) * p.block_size);
   const int t_full = min(ntiles, max(0, (wg_min - kb) / kKeyTile));
 
-  // S^T of one 32-key block for both query blocks: operands first, then MFMA
-  auto qk_block = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
-    bf16x8 a[KK];
+  // K operands (A of S^T = K.Q^T) of 32-key block kbk
+  auto read_k = [&](const char *buf, int kbk, bf16x8 (&a)[KK]) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) a[kk] = lds_read8(buf, koff[kk] + kbk * 32 * (2 * D));
+  };
+  // V operands (A of O^T += V^T.P^T) of 32-key block kbk
+  auto read_v = [&](const char *buf, int kbk, bf16x8 (&va)[2][DB]) {
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        va[mm][db] = lds_read8(buf, voff + (2 * kbk + mm) * Tile<D>::kPageBytes + db * 32 * (kPageSize * 2));
+  };
+  // S^T of one 32-key block for both query blocks
+  auto qk_mfma = [&](const bf16x8 (&a)[KK], f32x16 (&sc)[2]) {
     sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[0][0], f32x16{}, 0, 0, 0);
     sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[1][0], f32x16{}, 0, 0, 0);
 #pragma unroll
@@ -307,6 +336,11 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[0][kk], sc[0], 0, 0, 0);
       sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[1][kk], sc[1], 0, 0, 0);
     }
+  };
+  auto qk_block = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
+    bf16x8 a[KK];
+    read_k(buf, kbk, a);
+    qk_mfma(a, sc);
   };
   // keys at or past a row's limit get -inf
   auto mask_block = [&](int kblk0, f32x16 (&sc)[2]) {
@@ -329,30 +363,30 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   };
   // numerators 2^(s*scale*log2e - ref) to bf16 P^T, then O^T += V^T . P^T
-  auto softmax_pv = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
-    bf16x8 va[2][DB];
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-      for (int db = 0; db < DB; ++db) va[mm][db] = lds_read8(buf, voff[kbk][mm] + db * 32 * (kKeyTile * 2));
+  auto softmax_pv = [&](const bf16x8 (&va)[2][DB], f32x16 (&sc)[2]) {
     bf16x8 pb[2][2];    // [qb][m]: keys 16m + 8h .. +7 of this block
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       const float msafe = (m_ref[qb] == kNegInf) ? 0.f : m_ref[qb];
       float e[16];
-      float lsum = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][v], p.scale_log2, -msafe));
-        lsum += e[v];
-      }
-      l_run[qb] += lsum;
+      for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][v], p.scale_log2, -msafe));
+      // the row sum adds the bf16 numerators that enter P.V, two per dot2
+      float lsum = l_run[qb];
 #pragma unroll
       for (int mm = 0; mm < 2; ++mm) {
         const u32x4 w = {pack_bf16x2(e[8 * mm + 0], e[8 * mm + 1]), pack_bf16x2(e[8 * mm + 2], e[8 * mm + 3]),
                          pack_bf16x2(e[8 * mm + 4], e[8 * mm + 5]), pack_bf16x2(e[8 * mm + 6], e[8 * mm + 7])};
         pb[qb][mm] = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          // (copied out first: a bit cast of the vector element w[k] itself
+          // is compiled as a cast of w[0] by this compiler)
+          const uint32_t wk = w[k];
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wk), kOnes2, lsum, false);
+        }
       }
+      l_run[qb] = lsum;
     }
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm)
@@ -364,7 +398,10 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // ---- key loop: tile t lives in buffer t % 4; tiles t+1..t+3 are in flight
   // while tile t is computed.  pid holds the page ids of the next tile to load.
-  int pid[4];
+  const int wv = __builtin_amdgcn_readfirstlane(wave);   // wave index as a scalar
+  uint32_t kload_off[Tile<D>::kLoads];
+  k_load_offsets<D>(kload_off);
+  int pid = 0;                                             // this wave's page of the next tile
   auto buf_of = [&](int t) -> char * {
     switch (t & 3) {
       case 0: return lds0;
@@ -375,8 +412,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // direct loads of tile t into dst, then the page ids of tile t + 1
   auto issue = [&](int t, char *dst) {
-    load_tile<D>(p, g, pid, dst);
-    tile_pages(p, b, kb + (t + 1) * kKeyTile, pid);
+    load_tile<D>(p, g, wv, pid, kload_off, dst);
+    pid = wave_page(p, b, kb + (t + 1) * kKeyTile, wv);
   };
   constexpr int kLoadsPerTile = 2 * Tile<D>::kLoads;     // direct loads per thread per tile
   // waits until at most n tiles' loads of this thread are still in flight,
@@ -396,7 +433,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   };
   auto prologue = [&]() {
-    tile_pages(p, b, kb, pid);
+    pid = wave_page(p, b, kb, wv);
     for (int t = 0; t < 3 && t < ntiles; ++t) issue(t, buf_of(t));
     land(min(2, ntiles - 1));
     fix_tail(0);
@@ -410,8 +447,11 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       mask_block(key0, s0);
       mask_block(key0 + 32, s1);
     }
-    softmax_pv(buf, 0, s0);
-    softmax_pv(buf, 1, s1);
+    bf16x8 va[2][DB];
+    read_v(buf, 0, va);
+    softmax_pv(va, s0);
+    read_v(buf, 1, va);
+    softmax_pv(va, s1);
   };
   // one tile through dynamically chosen buffers (remainder, masked tiles)
   auto generic_step = [&](int t, bool masked) {
