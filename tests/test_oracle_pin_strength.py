@@ -11,12 +11,17 @@ import oracle
 oa = importlib.import_module("oracle.attention")
 oe = importlib.import_module("oracle.edit_select")   # the package re-exports a function of that name
 import oracle_pins as pins
+import oracle_pins_next as pins_next
+ou = importlib.import_module("oracle.update")
+oen = importlib.import_module("oracle.entropy")
+okv = importlib.import_module("oracle.kv_cache")
 
 
 def _mutant(module, old, new):
     src = inspect.getsource(module)
     assert src.count(old) == 1, f"mutation site not unique: {old!r}"
     m = types.ModuleType(module.__name__ + "_mutant")
+    m.__package__ = "oracle"          # relative imports resolve against the real package
     exec(compile(src.replace(old, new), "<mutant>", "exec"), m.__dict__)
     return m
 
@@ -74,3 +79,62 @@ def test_edit_mutant_is_caught(name):
 def test_unmutated_oracle_passes_all_pins():
     assert not _caught(pins.ATTENTION_CHECKS, oa)
     assert not _caught(pins.EDIT_CHECKS, oe)
+
+
+UPDATE_MUTATIONS = {
+    "Gamma uses >= instead of >": ("if conf[r] > om:", "if conf[r] >= om:"),
+    "force-unmask takes the last of equal confidences": ("if conf[r] > conf[best]:", "if conf[r] >= conf[best]:"),
+    "force-unmask even when Gamma is not empty": ("if m_rows and not any(action[r] == UNMASK for r in m_rows):",
+                                                  "if m_rows:"),
+    "no force-unmask": ("            action[best] = FORCE_UNMASK", "            pass"),
+    "edits masked rows too": ("        elif pred[r] != cur[r] and conf[r] >= oe:", "        if pred[r] != cur[r] and conf[r] >= oe:"),
+    "edit ignores the threshold": ("elif pred[r] != cur[r] and conf[r] >= oe:", "elif pred[r] != cur[r]:"),
+    "block flag from the first row only": ("1 if np.any(action[k * B:(k + 1) * B] != KEEP) else 0",
+                                           "1 if action[k * B] != KEEP else 0"),
+}
+
+
+@pytest.mark.parametrize("name", list(UPDATE_MUTATIONS))
+def test_update_mutant_is_caught(name):
+    old, new = UPDATE_MUTATIONS[name]
+    m = _mutant(ou, old, new)
+    assert _caught(pins_next.UPDATE_CHECKS, m), f"no pin catches: {name}"
+
+
+ENTROPY_MUTATIONS = {
+    "entropy without the log-sum-exp": ("logp = fin - lse", "logp = fin - mx"),
+    "entropy in bits": ("out[r] = -float(np.sum(np.exp(logp) * logp))", "out[r] = -float(np.sum(np.exp(logp) * logp)) / math.log(2.0)"),
+    "tail size rounded down": ("k = int(math.ceil(float(np.float32(rho)) * B))", "k = max(1, int(float(np.float32(rho)) * B))"),
+    "tail takes the smallest entropies": ("top = np.sort(e[i * B:(i + 1) * B])[::-1][:k]", "top = np.sort(e[i * B:(i + 1) * B])[:k]"),
+    "selection ties go to the latest block": ("if best == j or S[b, i] > S[b, best]:", "if best == j or S[b, i] >= S[b, best]:"),
+    "candidate window one block too wide": ("lo = max(0, j - int(k_max) + 1)", "lo = max(0, j - int(k_max))"),
+    "current block is a candidate": ("for i in range(lo, j):", "for i in range(lo, j + 1):"),
+}
+
+
+@pytest.mark.parametrize("name", list(ENTROPY_MUTATIONS))
+def test_entropy_mutant_is_caught(name):
+    old, new = ENTROPY_MUTATIONS[name]
+    m = _mutant(oen, old, new)
+    assert _caught(pins_next.ENTROPY_CHECKS, m), f"no pin catches: {name}"
+
+
+KV_MUTATIONS = {
+    "V written token-major": ("V[page, :, :, slot] = vn[row]", "V[page, :, slot % V.shape[2], :] = vn[row][:, :16]"),
+    "slot off by one": ("slot = pos % PAGE", "slot = (pos + 1) % PAGE"),
+    "positions relative to the page start": ("pos = int(st[b]) + t", "pos = t"),
+    "later-block mode refreshes nothing extra": ("elif seen and mode == REFRESH_CHANGED_AND_LATER:", "elif False:"),
+}
+
+
+@pytest.mark.parametrize("name", list(KV_MUTATIONS))
+def test_kv_mutant_is_caught(name):
+    old, new = KV_MUTATIONS[name]
+    m = _mutant(okv, old, new)
+    assert _caught(pins_next.KV_CHECKS, m), f"no pin catches: {name}"
+
+
+def test_unmutated_next_oracle_passes_all_pins():
+    assert not _caught(pins_next.UPDATE_CHECKS, ou)
+    assert not _caught(pins_next.ENTROPY_CHECKS, oen)
+    assert not _caught(pins_next.KV_CHECKS, okv)
