@@ -217,6 +217,69 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
     print("\n".join(lines))
 
 
+def _time_events(fn, n):
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(n):
+        fn()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    return ev[0].elapsed_time(ev[1]) / n / 1e3
+
+
+def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
+    """Times the calls outside the timed step: the full threshold update with
+    entropy on the step's logits (every 32 rows a block, 40% of rows masked),
+    the K/V write-back of the window (all sequences, every window token), and
+    tail-entropy scores plus start-block choice for every sequence."""
+    import torch
+    dev = logits.device
+    B = 32
+    g = torch.Generator(device="cpu").manual_seed(5)
+    cur_m = cur.clone()
+    masked = torch.rand(R, generator=g) < 0.4
+    cur_m[masked.to(dev)] = V - 1
+    out = mbe.threshold_update(logits, cur_m, V - 1, B, 0.5, 0.0, with_entropy=True)
+    t_upd = _time_events(lambda: mbe.threshold_update(logits, cur_m, V - 1, B, 0.5, 0.0, with_entropy=True,
+                                                      out=out), steps)
+    upd_bytes = R * V * 2 + R * (4 + 4 + 4 + 1 + 4) + R // B
+    # refresh write-back of every window token (k blocks per sequence)
+    P = attn_case.prefix_lens.to(dev)
+    W = attn_case.window_lens.to(dev)
+    Hkv, D = attn_case.num_kv_heads, attn_case.head_dim
+    T = int(attn_case.window_lens.sum())
+    kn = torch.randn(T, Hkv, D, generator=g).to(torch.bfloat16).to(dev)
+    vn = torch.randn(T, Hkv, D, generator=g).to(torch.bfloat16).to(dev)
+    kp, vp = c.k_pages.clone(), c.v_pages.clone()       # keep the step's pools intact
+    max_w = int(attn_case.window_lens.max())
+    t_kv = _time_events(lambda: mbe.kv_write(kp, vp, c.page_table, P, W, kn, vn, max_len=max_w), steps)
+    del kp, vp
+    kv_bytes = 2 * 2 * T * Hkv * D * 2
+    # tail scores of the step's rows and one start block per sequence
+    ent = out["entropy"]
+    scores = mbe.tail_entropy_scores(ent, B, 0.25)
+    nb = scores.shape[0] // attn_case.batch
+    sc2 = scores[: nb * attn_case.batch].view(attn_case.batch, nb)
+    jcur = torch.full((attn_case.batch,), nb, dtype=torch.int32, device=dev)
+    t_tail = _time_events(lambda: mbe.tail_entropy_scores(ent, B, 0.25, out=scores), steps)
+    t_sel = _time_events(lambda: mbe.select_start_block(sc2, jcur, 4), steps)
+    return {
+        "threshold_update": {"ms": round(t_upd * 1e3, 4), "rows": R, "vocab": V, "block": B,
+                             "with_entropy": True, "algorithmic_mb": round(upd_bytes / 1e6, 1),
+                             "gbs": round(upd_bytes / t_upd / 1e9, 1),
+                             "pct_hbm_peak": round(100 * upd_bytes / t_upd / 1e9 / PEAK_HBM_GBS, 2)},
+        "kv_write": {"ms": round(t_kv * 1e3, 4), "tokens": T, "kv_heads": Hkv, "head_dim": D,
+                     "algorithmic_mb": round(kv_bytes / 1e6, 2), "gbs": round(kv_bytes / t_kv / 1e9, 1)},
+        "tail_entropy_scores": {"ms": round(t_tail * 1e3, 4), "blocks": int(scores.shape[0])},
+        "select_start_block": {"ms": round(t_sel * 1e3, 4), "sequences": attn_case.batch},
+    }
+
+
 def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_sample, edit_sample):
     """Times the fp64 oracle (as it stands) on a bounded sample of the same
     workload on the host cores, scaled to the whole step."""
@@ -269,6 +332,7 @@ def main():
     ap.add_argument("--k", type=int, default=None, help="window blocks (span sweep workload)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
     ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
@@ -408,6 +472,8 @@ def main():
                      "traffic_detail": traffic, "algorithmic_bytes": attn_bytes},
         "wall_s": round(wall, 3),
     }
+    if edit_case is not None and not args.no_next:
+        res["next_rows"] = bench_next_rows(mbe, attn_case, c, logits, cur, R, V, args.steps)
     if not args.no_cpu_baseline and edit_case is not None:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl, attn_case, edit_case, flops, e_bytes,

@@ -24,8 +24,9 @@
  *     error string in mbe_last_error().
  *   - No global mutable state except the thread-local error string.  Calls
  *     that share a workspace must not overlap in time.
- *   - One call launches one kernel, plus a small merge/finalize kernel when
- *     the work is split across workgroups (see the workspace sizes).
+ *   - The attention and edit-selection calls launch one kernel, plus a small
+ *     merge/finalize kernel when the work is split across workgroups (see the
+ *     workspace sizes).  mbe_threshold_update adds one per-block kernel.
  */
 #ifndef MBE_H_
 #define MBE_H_
@@ -162,6 +163,85 @@ mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int6
 /* Workspace bytes mbe_edit_select needs for rows x vocab (0 = none).
  * Returns (size_t)-1 for negative sizes. */
 size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab);
+
+/* ---------------------------------------------------------------------------
+ * Full threshold update (paper, Sec. "Configurable threshold decoding",
+ * Eq. (1) and the force-unmask rule after it).  Rows form blocks of
+ * block_size consecutive rows (row r belongs to block r / block_size).  With
+ * a = lowest index of the row maximum and conf[r] its softmax probability (as
+ * in mbe_edit_select), each row gets an action:
+ *   MBE_UNMASK        cur == mask_id and conf > omega_mask          (Gamma_t)
+ *   MBE_FORCE_UNMASK  cur == mask_id, no row of its block is MBE_UNMASK, and
+ *                     it has the highest conf among the block's masked rows
+ *                     (the lowest such row on ties)
+ *   MBE_EDIT          cur != mask_id, a != cur and conf >= omega_edit (Delta_t,
+ *                     the edit rule of mbe_edit_select)
+ *   MBE_KEEP          otherwise
+ * new_tokens[r] = a for every action but MBE_KEEP, cur otherwise.
+ * block_changed[k] = 1 when some row of block k has an action other than
+ * MBE_KEEP.  changed_count (device int32, may be NULL) receives the number of
+ * such rows, so a loop of editing passes can stop when it reaches 0 without
+ * copying per-row results to the host.  entropy (may be NULL) receives each
+ * row's softmax entropy in nats, -sum_v p_v ln p_v, computed in the same pass
+ * over the logits (the input of the tail-entropy selection below).
+ * rows must be a multiple of block_size.  logits/threshold contract as for
+ * mbe_edit_select.  workspace: mbe_threshold_update_workspace_size bytes,
+ * 256-byte aligned, any contents.  MBE_ERR_BAD_VALUE for a NaN threshold. */
+typedef enum { MBE_KEEP = 0, MBE_UNMASK = 1, MBE_FORCE_UNMASK = 2, MBE_EDIT = 3 } mbe_action;
+
+mbe_status mbe_threshold_update(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                const int32_t *cur_tokens, int32_t mask_id, int32_t block_size,
+                                float omega_mask, float omega_edit, int32_t *new_tokens, float *conf,
+                                uint8_t *action, uint8_t *block_changed, int32_t *changed_count,
+                                float *entropy, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes mbe_threshold_update needs (the per-row predictions plus
+ * the per-chunk partials of mbe_edit_select).  (size_t)-1 for negative sizes. */
+size_t mbe_threshold_update_workspace_size(int64_t rows, int64_t vocab);
+
+/* Tail-entropy score of every block (paper, Sec. "Training-Free MBE
+ * Decoding", Eq. (5)): scores[k] = mean of the ceil(rho * block_size) largest
+ * entropy values of rows k*block_size .. (k+1)*block_size - 1.  The values are
+ * summed from the largest down, so the result does not depend on launch
+ * shape.  1 <= block_size <= 1024 and 1 <= ceil(rho * block_size) <= block_size. */
+mbe_status mbe_tail_entropy_scores(const float *entropy, int64_t num_blocks, int32_t block_size,
+                                   float rho, float *scores, void *stream);
+
+/* Start block of every sequence's editing window (Eq. (6)): with
+ * j = current_block[b], start_block[b] = the block i in
+ * [max(0, j - k_max + 1), j) with the highest scores[b * score_stride + i];
+ * the earliest such block on ties (the widest window); j itself when j = 0.
+ * current_block values are clamped to [0, score_stride]. */
+mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t score_stride,
+                                  const int32_t *current_block, int32_t k_max, int32_t *start_block,
+                                  void *stream);
+
+/* Write-back of recomputed K/V (paper, Sec. "Infrastructure Optimization",
+ * cache control: after editing, changed blocks are recomputed under standard
+ * attention and their K/V restore the cache).  Token t < lens[b] of sequence
+ * b (rows of sequence b start at sum_{b' < b} lens[b']) is written at
+ * absolute position start_pos[b] + t, i.e. slot (position % 16) of page
+ * page_table[b][position / 16], for every KV head:
+ *   k_pages[page][head][slot][:] = k_new[row][head][:]      (bf16)
+ *   v_pages[page][head][:][slot] = v_new[row][head][:]      (token-minor pool)
+ * k_new/v_new: bf16 [total_tokens][num_kv_heads][head_dim]; max_len bounds
+ * every lens[b] (host-known, sizes the grid).  Other slots are not touched.
+ * Positions must lie inside the sequence's page table row (a precondition;
+ * page ids are clamped into the pool). */
+mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads,
+                        int32_t head_dim, const int32_t *page_table, int32_t max_pages_per_seq,
+                        const int32_t *start_pos, const int32_t *lens, int32_t batch, int32_t max_len,
+                        int32_t total_tokens, const void *k_new, const void *v_new, void *stream);
+
+/* Blocks to recompute after editing, from the per-block changed flags
+ * ([batch][num_blocks], e.g. block_changed of mbe_threshold_update laid out
+ * per sequence).  MBE_REFRESH_CHANGED: exactly the changed blocks, as the
+ * paper describes.  MBE_REFRESH_CHANGED_AND_LATER: also every block after the
+ * first changed one, whose standard-scope K/V attended to the old tokens. */
+typedef enum { MBE_REFRESH_CHANGED = 0, MBE_REFRESH_CHANGED_AND_LATER = 1 } mbe_refresh_mode;
+
+mbe_status mbe_refresh_blocks(const uint8_t *block_changed, int32_t batch, int32_t num_blocks,
+                              int32_t mode, uint8_t *refresh, void *stream);
 
 /* Static description of a status code. */
 const char *mbe_status_string(mbe_status s);

@@ -26,7 +26,11 @@ STATUS_NAMES = {0: "MBE_OK", 1: "MBE_ERR_NULL_ARG", 2: "MBE_ERR_BAD_SHAPE", 3: "
 MASK_MODES = {"bidir": 0, "block_causal": 1}
 
 EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
-           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_status_string", "mbe_last_error")
+           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_threshold_update",
+           "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores", "mbe_select_start_block",
+           "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error")
+ACTIONS = {"keep": 0, "unmask": 1, "force_unmask": 2, "edit": 3}
+REFRESH_MODES = {"changed": 0, "changed_and_later": 1}
 
 
 class MbeError(RuntimeError):
@@ -82,6 +86,20 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_edit_select.restype = ctypes.c_int
         lib.mbe_edit_select_workspace_size.argtypes = [i64, i64]
         lib.mbe_edit_select_workspace_size.restype = sz
+        f32 = ctypes.c_float
+        lib.mbe_threshold_update.argtypes = [vp, i64, i64, i64, vp, i32, i32, f32, f32, vp, vp, vp, vp, vp, vp, vp,
+                                             sz, vp]
+        lib.mbe_threshold_update.restype = ctypes.c_int
+        lib.mbe_threshold_update_workspace_size.argtypes = [i64, i64]
+        lib.mbe_threshold_update_workspace_size.restype = sz
+        lib.mbe_tail_entropy_scores.argtypes = [vp, i64, i32, f32, vp, vp]
+        lib.mbe_tail_entropy_scores.restype = ctypes.c_int
+        lib.mbe_select_start_block.argtypes = [vp, i32, i32, vp, i32, vp, vp]
+        lib.mbe_select_start_block.restype = ctypes.c_int
+        lib.mbe_kv_write.argtypes = [vp, vp, i32, i32, i32, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
+        lib.mbe_kv_write.restype = ctypes.c_int
+        lib.mbe_refresh_blocks.argtypes = [vp, i32, i32, i32, vp, vp]
+        lib.mbe_refresh_blocks.restype = ctypes.c_int
         lib.mbe_status_string.argtypes = [ctypes.c_int]
         lib.mbe_status_string.restype = ctypes.c_char_p
         lib.mbe_last_error.argtypes = []
@@ -264,3 +282,100 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
         _ptr(logits), rows, v, ld, _ptr(cur_tokens), ctypes.c_float(threshold), _ptr(new), _ptr(conf),
         _ptr(changed), _ptr(ws), need if ws is not None else 0, stream))
     return new, conf, changed
+
+
+def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_edit, *, vocab=None,
+                     with_entropy=False, out=None):
+    """Full threshold update (paper, Eq. (1) with force-unmask).  Rows form
+    blocks of block_size consecutive rows.  Returns a dict of device tensors:
+    new_tokens int32, conf float32, action uint8 (ACTIONS), block_changed
+    uint8 [rows / block_size], changed_count int32 [1] and, when asked,
+    entropy float32 (nats)."""
+    lib = load()
+    dev = logits.device
+    _need(cur_tokens, "cur_tokens", torch.int32, dev, 1)
+    if logits.dtype != torch.bfloat16 or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a bf16 [rows, row_stride] tensor with unit column stride")
+    rows = logits.shape[0]
+    if cur_tokens.shape[0] != rows:
+        raise ValueError("cur_tokens must have one entry per row")
+    v = logits.shape[1] if vocab is None else int(vocab)
+    ld = logits.stride(0) if rows > 1 else max(logits.shape[1], 1)
+    nblk = rows // block_size if block_size > 0 else 0
+    if out is None:
+        out = {"new_tokens": torch.empty(rows, dtype=torch.int32, device=dev),
+               "conf": torch.empty(rows, dtype=torch.float32, device=dev),
+               "action": torch.empty(rows, dtype=torch.uint8, device=dev),
+               "block_changed": torch.empty(max(nblk, 1), dtype=torch.uint8, device=dev),
+               "changed_count": torch.empty(1, dtype=torch.int32, device=dev)}
+        if with_entropy:
+            out["entropy"] = torch.empty(rows, dtype=torch.float32, device=dev)
+    need = lib.mbe_threshold_update_workspace_size(rows, v)
+    ws = _workspace("update", dev, need if need != ctypes.c_size_t(-1).value else 0)
+    _check("mbe_threshold_update", lib.mbe_threshold_update(
+        _ptr(logits), rows, v, ld, _ptr(cur_tokens), int(mask_id), int(block_size), ctypes.c_float(omega_mask),
+        ctypes.c_float(omega_edit), _ptr(out["new_tokens"]), _ptr(out["conf"]), _ptr(out["action"]),
+        _ptr(out["block_changed"]), _ptr(out.get("changed_count")), _ptr(out.get("entropy")), _ptr(ws),
+        need if ws is not None else 0, _stream(dev)))
+    return out
+
+
+def tail_entropy_scores(entropy, block_size, rho, *, out=None):
+    """Eq. (5): mean of the ceil(rho * B) largest entropies of every block of
+    block_size consecutive rows.  entropy: float32 [num_blocks * B]."""
+    lib = load()
+    dev = entropy.device
+    _need(entropy, "entropy", torch.float32, dev, 1)
+    nblk = entropy.shape[0] // block_size if block_size > 0 else 0
+    scores = torch.empty(nblk, dtype=torch.float32, device=dev) if out is None else out
+    _check("mbe_tail_entropy_scores", lib.mbe_tail_entropy_scores(
+        _ptr(entropy), nblk, int(block_size), ctypes.c_float(rho), _ptr(scores), _stream(dev)))
+    return scores
+
+
+def select_start_block(scores, current_block, k_max, *, out=None):
+    """Eq. (6): start block of every sequence's window.  scores: float32
+    [batch, max_blocks]; current_block: int32 [batch]."""
+    lib = load()
+    dev = scores.device
+    _need(scores, "scores", torch.float32, dev, 2)
+    _need(current_block, "current_block", torch.int32, dev, 1)
+    batch = current_block.shape[0]
+    start = torch.empty(batch, dtype=torch.int32, device=dev) if out is None else out
+    _check("mbe_select_start_block", lib.mbe_select_start_block(
+        _ptr(scores), batch, scores.shape[1], _ptr(current_block), int(k_max), _ptr(start), _stream(dev)))
+    return start
+
+
+def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max_len=None):
+    """Write recomputed K/V (bf16 [total_tokens, heads, D]) into the paged
+    pools in place: token t of sequence b goes to position start_pos[b] + t."""
+    lib = load()
+    dev = k_pages.device
+    _need(k_pages, "k_pages", torch.bfloat16, dev, 4)
+    _need(v_pages, "v_pages", torch.bfloat16, dev, 4)
+    _need(page_table, "page_table", torch.int32, dev, 2)
+    _need(start_pos, "start_pos", torch.int32, dev, 1)
+    _need(lens, "lens", torch.int32, dev, 1)
+    _need(k_new, "k_new", torch.bfloat16, dev, 3)
+    _need(v_new, "v_new", torch.bfloat16, dev, 3)
+    batch = start_pos.shape[0]
+    if max_len is None:
+        max_len = int(lens.max().item()) if batch else 0
+    _check("mbe_kv_write", lib.mbe_kv_write(
+        _ptr(k_pages), _ptr(v_pages), k_pages.shape[0], k_pages.shape[1], k_pages.shape[3], _ptr(page_table),
+        page_table.shape[1], _ptr(start_pos), _ptr(lens), batch, int(max_len), k_new.shape[0], _ptr(k_new),
+        _ptr(v_new), _stream(dev)))
+
+
+def refresh_blocks(block_changed, mode="changed", *, out=None):
+    """Blocks to recompute after editing from per-block changed flags
+    (uint8 [batch, num_blocks]); mode "changed" or "changed_and_later"."""
+    lib = load()
+    dev = block_changed.device
+    _need(block_changed, "block_changed", torch.uint8, dev, 2)
+    refresh = torch.empty_like(block_changed) if out is None else out
+    _check("mbe_refresh_blocks", lib.mbe_refresh_blocks(
+        _ptr(block_changed), block_changed.shape[0], block_changed.shape[1], REFRESH_MODES[mode], _ptr(refresh),
+        _stream(dev)))
+    return refresh

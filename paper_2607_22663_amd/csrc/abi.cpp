@@ -333,6 +333,155 @@ mbe_status mbe_edit_select(const void *logits, int64_t rows, int64_t vocab, int6
   return MBE_OK;
 }
 
+size_t mbe_threshold_update_workspace_size(int64_t rows, int64_t vocab) {
+  if (rows < 0 || vocab < 0) return static_cast<size_t>(-1);
+  if (rows == 0) return 0;
+  const size_t partials = mbe_edit_select_workspace_size(rows, vocab);
+  return align_up(static_cast<size_t>(rows) * sizeof(int32_t)) + partials;   // predictions, then partials
+}
+
+mbe_status mbe_threshold_update(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                const int32_t *cur_tokens, int32_t mask_id, int32_t block_size, float omega_mask,
+                                float omega_edit, int32_t *new_tokens, float *conf, uint8_t *action,
+                                uint8_t *block_changed, int32_t *changed_count, float *entropy, void *workspace,
+                                size_t workspace_bytes, void *stream) {
+  if (rows < 0 || vocab < 0) return fail(MBE_ERR_BAD_SHAPE, "rows %lld / vocab %lld negative",
+                                         static_cast<long long>(rows), static_cast<long long>(vocab));
+  if (rows > 0 && vocab < 1) return fail(MBE_ERR_BAD_SHAPE, "vocab must be >= 1");
+  if (row_stride < vocab)
+    return fail(MBE_ERR_BAD_SHAPE, "row_stride %lld < vocab %lld", static_cast<long long>(row_stride),
+                static_cast<long long>(vocab));
+  if (vocab > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "vocab beyond int32 indices");
+  if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
+  if (rows % block_size != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "rows %lld is not a multiple of block_size %d", static_cast<long long>(rows),
+                block_size);
+  if (omega_mask != omega_mask || omega_edit != omega_edit) return fail(MBE_ERR_BAD_VALUE, "threshold is NaN");
+  if (rows == 0) return MBE_OK;
+  if (!logits || !cur_tokens || !new_tokens || !conf || !action || !block_changed)
+    return fail(MBE_ERR_NULL_ARG, "logits, cur_tokens, new_tokens, conf, action and block_changed must be non-NULL");
+  int32_t chunks;
+  int64_t len;
+  mbe::edit_select_plan(rows, vocab, &chunks, &len);
+  if (rows * chunks > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "too many rows");
+  const size_t need = mbe_threshold_update_workspace_size(rows, vocab);
+  if (!workspace) return fail(MBE_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+  if (workspace_bytes < need)
+    return fail(MBE_ERR_WORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(MBE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  mbe::EsParams p{};
+  p.logits = static_cast<const uint16_t *>(logits);
+  p.rows = rows;
+  p.vocab = vocab;
+  p.ld = row_stride;
+  p.chunk_len = len;
+  p.chunks = chunks;
+  p.update = 1;
+  p.cur = cur_tokens;
+  p.threshold = omega_edit;
+  p.new_tokens = new_tokens;
+  p.conf = conf;
+  char *ws = static_cast<char *>(workspace);
+  p.pred = reinterpret_cast<int32_t *>(ws);
+  if (chunks > 1) p.partials = reinterpret_cast<mbe::EsPartial *>(ws + align_up(static_cast<size_t>(rows) * 4));
+  p.entropy = entropy;
+  p.changed_count = changed_count;
+  p.action = action;
+  p.block_changed = block_changed;
+  p.mask_id = mask_id;
+  p.block_size = block_size;
+  p.omega_mask = omega_mask;
+  const bool vec = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && (row_stride % 8 == 0);
+  hipError_t e = mbe::launch_threshold_update(p, vec, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "threshold update launch");
+  return MBE_OK;
+}
+
+mbe_status mbe_tail_entropy_scores(const float *entropy, int64_t num_blocks, int32_t block_size, float rho,
+                                   float *scores, void *stream) {
+  if (num_blocks < 0) return fail(MBE_ERR_BAD_SHAPE, "num_blocks %lld < 0", static_cast<long long>(num_blocks));
+  if (block_size < 1 || block_size > 1024)
+    return fail(MBE_ERR_UNSUPPORTED, "block_size %d outside [1, 1024]", block_size);
+  if (!(rho > 0.f) || rho > 1.f) return fail(MBE_ERR_BAD_VALUE, "rho %g outside (0, 1]", static_cast<double>(rho));
+  // k = ceil(rho * B), computed in double from the fp32 rho
+  const double kd = std::ceil(static_cast<double>(rho) * block_size);
+  const int32_t k = static_cast<int32_t>(kd);
+  if (k < 1 || k > block_size) return fail(MBE_ERR_BAD_VALUE, "ceil(rho * block_size) = %d", k);
+  if (num_blocks > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "too many blocks");
+  if (num_blocks == 0) return MBE_OK;
+  if (!entropy || !scores) return fail(MBE_ERR_NULL_ARG, "entropy and scores must be non-NULL");
+  hipError_t e = mbe::launch_tail_entropy_scores(entropy, num_blocks, block_size, k, scores,
+                                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "tail entropy launch");
+  return MBE_OK;
+}
+
+mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t score_stride,
+                                  const int32_t *current_block, int32_t k_max, int32_t *start_block, void *stream) {
+  if (batch < 0) return fail(MBE_ERR_BAD_SHAPE, "batch %d < 0", batch);
+  if (score_stride < 0) return fail(MBE_ERR_BAD_SHAPE, "score_stride %d < 0", score_stride);
+  if (k_max < 1) return fail(MBE_ERR_BAD_SHAPE, "k_max %d < 1", k_max);
+  if (batch == 0) return MBE_OK;
+  if (!current_block || !start_block || (score_stride > 0 && !scores))
+    return fail(MBE_ERR_NULL_ARG, "scores, current_block and start_block must be non-NULL");
+  hipError_t e = mbe::launch_select_start_block(scores, batch, score_stride, current_block, k_max, start_block,
+                                                static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "start block launch");
+  return MBE_OK;
+}
+
+mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads, int32_t head_dim,
+                        const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *start_pos,
+                        const int32_t *lens, int32_t batch, int32_t max_len, int32_t total_tokens, const void *k_new,
+                        const void *v_new, void *stream) {
+  if (head_dim != 64 && head_dim != 128)
+    return fail(MBE_ERR_UNSUPPORTED, "head_dim %d: supported are 64 and 128", head_dim);
+  if (num_kv_heads < 1 || num_kv_heads > 65535) return fail(MBE_ERR_BAD_SHAPE, "num_kv_heads %d", num_kv_heads);
+  if (batch < 0 || batch > 65535) return fail(MBE_ERR_BAD_SHAPE, "batch %d outside [0, 65535]", batch);
+  if (max_len < 0 || total_tokens < 0 || num_pages < 0 || max_pages_per_seq < 0)
+    return fail(MBE_ERR_BAD_SHAPE, "negative max_len/total_tokens/num_pages/max_pages_per_seq");
+  if (batch == 0 || max_len == 0 || total_tokens == 0) return MBE_OK;
+  if (num_pages < 1 || max_pages_per_seq < 1) return fail(MBE_ERR_BAD_SHAPE, "empty page pool or table");
+  if (!k_pages || !v_pages || !page_table || !start_pos || !lens || !k_new || !v_new)
+    return fail(MBE_ERR_NULL_ARG, "pools, page_table, start_pos, lens, k_new and v_new must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(k_pages) | reinterpret_cast<uintptr_t>(v_pages) |
+       reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new)) % 16 != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "pools and k_new/v_new must be 16-byte aligned");
+  mbe::KvWriteParams p{};
+  p.k_pages = static_cast<uint16_t *>(k_pages);
+  p.v_pages = static_cast<uint16_t *>(v_pages);
+  p.num_pages = num_pages;
+  p.num_kv_heads = num_kv_heads;
+  p.head_dim = head_dim;
+  p.page_table = page_table;
+  p.max_pages = max_pages_per_seq;
+  p.start_pos = start_pos;
+  p.lens = lens;
+  p.batch = batch;
+  p.max_len = max_len;
+  p.total_tokens = total_tokens;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  hipError_t e = mbe::launch_kv_write(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kv write launch");
+  return MBE_OK;
+}
+
+mbe_status mbe_refresh_blocks(const uint8_t *block_changed, int32_t batch, int32_t num_blocks, int32_t mode,
+                              uint8_t *refresh, void *stream) {
+  if (batch < 0 || num_blocks < 0) return fail(MBE_ERR_BAD_SHAPE, "batch %d / num_blocks %d negative", batch,
+                                               num_blocks);
+  if (mode != MBE_REFRESH_CHANGED && mode != MBE_REFRESH_CHANGED_AND_LATER)
+    return fail(MBE_ERR_UNSUPPORTED, "refresh mode %d", mode);
+  if (batch == 0 || num_blocks == 0) return MBE_OK;
+  if (!block_changed || !refresh) return fail(MBE_ERR_NULL_ARG, "block_changed and refresh must be non-NULL");
+  hipError_t e = mbe::launch_refresh_blocks(block_changed, batch, num_blocks, mode, refresh,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "refresh launch");
+  return MBE_OK;
+}
+
 const char *mbe_status_string(mbe_status s) {
   switch (s) {
     case MBE_OK: return "ok";

@@ -40,24 +40,47 @@ __device__ __forceinline__ float bf16_at(const uint16_t *p) {
   return __uint_as_float(static_cast<uint32_t>(*p) << 16);
 }
 
-// exp(d) for d <= 0 through the hardware base-2 exponential.
-__device__ __forceinline__ float exp_neg(float d) { return __builtin_amdgcn_exp2f(d * kLog2e); }
+// Exponent arguments below this are exactly 0 after exp2 in fp32; clamping
+// there keeps 0 * (-inf) out of the entropy sum.
+constexpr float kYMin = -256.f;
 
-// Merge partial (m, s) with (m2, s2): the sums are rescaled to the common max.
-__device__ __forceinline__ void merge_ms(float &m, float &s, float m2, float s2) {
+// Merge partial (m, s, t) with (m2, s2, t2): the sums are rescaled to the
+// common max M.  With d = (m - M) log2(e): s -> 2^d s, t -> 2^d (t + d s).
+template <bool ENT>
+__device__ __forceinline__ void merge_ms(float &m, float &s, float &t, float m2, float s2, float t2) {
   const float M = fmaxf(m, m2);
   if (M == -INFINITY) return;     // both empty so far
-  const float a = (m == -INFINITY) ? 0.f : s * exp_neg(m - M);
-  const float b = (m2 == -INFINITY) ? 0.f : s2 * exp_neg(m2 - M);
+  float a = 0.f, b = 0.f, ta = 0.f, tb = 0.f;
+  if (m != -INFINITY) {
+    const float d = (m - M) * kLog2e;
+    const float f = __builtin_amdgcn_exp2f(d);
+    a = s * f;
+    if (ENT) ta = f * __builtin_fmaf(d, s, t);
+  }
+  if (m2 != -INFINITY) {
+    const float d = (m2 - M) * kLog2e;
+    const float f = __builtin_amdgcn_exp2f(d);
+    b = s2 * f;
+    if (ENT) tb = f * __builtin_fmaf(d, s2, t2);
+  }
   s = a + b;
+  if (ENT) t = ta + tb;
   m = M;
 }
 
-// Merge partial (m, s, i) with (m2, s2, i2): larger max wins, equal maxima keep
-// the lower index.
-__device__ __forceinline__ void merge(float &m, float &s, int32_t &i, float m2, float s2, int32_t i2) {
+// Merge partial (m, s, t, i) with (m2, s2, t2, i2): larger max wins, equal
+// maxima keep the lower index.
+template <bool ENT>
+__device__ __forceinline__ void merge(float &m, float &s, float &t, int32_t &i, float m2, float s2, float t2,
+                                      int32_t i2) {
   i = (m > m2) ? i : ((m2 > m) ? i2 : min(i, i2));
-  merge_ms(m, s, m2, s2);
+  merge_ms<ENT>(m, s, t, m2, s2, t2);
+}
+
+// Entropy in nats from s = sum 2^y and t = sum 2^y y:
+// H = -sum p ln p with p = 2^y / s, i.e. ln 2 (log2 s - t / s).
+__device__ __forceinline__ float entropy_nats(float s, float t) {
+  return 0.69314718055994531f * (log2f(s) - t / s);
 }
 
 // Loads vector unit `unit` (elements 8*unit .. 8*unit+7) as 8 floats; elements
@@ -79,21 +102,31 @@ __device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int
   }
 }
 
-// The token-to-token decision for one row from its (max, argmax, sum).
-__device__ __forceinline__ void decide(const EsParams &p, int64_t row, float m, float s, int32_t idx) {
-  const int32_t cur = p.cur[row];
+// The token-to-token decision for one row from its (max, argmax, sum), or,
+// for the threshold update, the row's prediction, confidence and entropy.
+template <bool ENT>
+__device__ __forceinline__ void decide(const EsParams &p, int64_t row, float m, float s, float t, int32_t idx) {
   const float conf = 1.0f / s;          // correctly rounded division
+  if (p.update) {
+    p.pred[row] = idx;
+    p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
+    if (ENT) p.entropy[row] = entropy_nats(s, t);
+    return;
+  }
+  const int32_t cur = p.cur[row];
   const bool change = (m != -INFINITY) && (idx != cur) && (conf >= p.threshold);
   p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
   p.new_tokens[row] = change ? idx : cur;
   p.changed[row] = change ? 1 : 0;
 }
 
-template <bool VEC>
+template <bool VEC, bool ENT>
 __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   __shared__ float sh_m[kT / 64];
   __shared__ float sh_s[kT / 64];
+  __shared__ float sh_t[kT / 64];
   __shared__ int32_t sh_i[kT / 64];
+  if (p.changed_count && blockIdx.x == 0 && threadIdx.x == 0) *p.changed_count = 0;   // counted per block later
 
   const int64_t wg = blockIdx.x;
   const int64_t row = wg / p.chunks;
@@ -105,7 +138,7 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   const int64_t u0 = c0 / 8;
   const int64_t u1 = (c1 + 7) / 8;
 
-  float m = -INFINITY, s = 0.f;
+  float m = -INFINITY, s = 0.f, t = 0.f;
   int32_t it_max = -1;
   int32_t it = 0;
   for (int64_t base = u0; base < u1; base += kT * kU, ++it) {
@@ -126,17 +159,31 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
 #pragma unroll
       for (int k = 0; k < 8; k += 2) cm = fmaxf(cm, fmaxf(x[j][k], x[j][k + 1]));
     if (cm > m) {
-      s = (m == -INFINITY) ? 0.f : s * exp_neg(m - cm);
+      if (m == -INFINITY) {
+        s = 0.f;
+        t = 0.f;
+      } else {
+        const float d = (m - cm) * kLog2e;
+        const float f = __builtin_amdgcn_exp2f(d);
+        if (ENT) t = f * __builtin_fmaf(d, s, t);
+        s *= f;
+      }
       m = cm;
       it_max = it;
     }
     const float ms = (m == -INFINITY) ? 0.f : m;
-    float acc = 0.f;
+    float acc = 0.f, acct = 0.f;
 #pragma unroll
     for (int j = 0; j < kU; ++j)
 #pragma unroll
-      for (int k = 0; k < 8; ++k) acc += exp_neg(x[j][k] - ms);
+      for (int k = 0; k < 8; ++k) {
+        const float y = (x[j][k] - ms) * kLog2e;
+        const float e = __builtin_amdgcn_exp2f(y);
+        acc += e;
+        if (ENT) acct = __builtin_fmaf(e, fmaxf(y, kYMin), acct);
+      }
     s += acc;
+    if (ENT) t += acct;
   }
 
   // (max, rescaled sum) over the workgroup: wave butterfly, then the four
@@ -146,18 +193,21 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   for (int o = 32; o >= 1; o >>= 1) {
     const float m2 = __shfl_xor(m, o);
     const float s2 = __shfl_xor(s, o);
-    merge_ms(m, s, m2, s2);
+    const float t2 = ENT ? __shfl_xor(t, o) : 0.f;
+    merge_ms<ENT>(m, s, t, m2, s2, t2);
   }
   const int wave = tid / 64;
   if ((tid & 63) == 0) {
     sh_m[wave] = m;
     sh_s[wave] = s;
+    sh_t[wave] = t;
   }
   __syncthreads();
   m = sh_m[0];
   s = sh_s[0];
+  t = sh_t[0];
 #pragma unroll
-  for (int w = 1; w < kT / 64; ++w) merge_ms(m, s, sh_m[w], sh_s[w]);
+  for (int w = 1; w < kT / 64; ++w) merge_ms<ENT>(m, s, t, sh_m[w], sh_s[w], sh_t[w]);
 
   // First index of the chunk maximum.  Only threads whose own maximum equals
   // it look: their first occurrence lies in iteration it_max, re-read once
@@ -188,22 +238,79 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   for (int w = 0; w < kT / 64; ++w) idx = min(idx, sh_i[w]);
 
   if (p.chunks > 1) {     // merged by the finalize kernel
-    p.partials[row * p.chunks + chunk] = EsPartial{m, s, idx, 0};
+    p.partials[row * p.chunks + chunk] = EsPartial{m, s, idx, t};
     return;
   }
-  decide(p, row, m, s, idx);
+  decide<ENT>(p, row, m, s, t, idx);
 }
 
 // Rows reduced in several chunks: one thread per row merges the chunk
 // partials in chunk order (the kernel boundary makes them visible).
+template <bool ENT>
 __global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (row >= p.rows) return;
   const EsPartial *pp = p.partials + row * p.chunks;
-  float m = pp[0].m, s = pp[0].s;
+  float m = pp[0].m, s = pp[0].s, t = pp[0].t;
   int32_t idx = pp[0].idx;
-  for (int c = 1; c < p.chunks; ++c) merge(m, s, idx, pp[c].m, pp[c].s, pp[c].idx);
-  decide(p, row, m, s, idx);
+  for (int c = 1; c < p.chunks; ++c) merge<ENT>(m, s, t, idx, pp[c].m, pp[c].s, pp[c].t, pp[c].idx);
+  decide<ENT>(p, row, m, s, t, idx);
+}
+
+// Threshold update, second step: one workgroup per block of block_size rows
+// applies the mask-to-token set, the force-unmask and the token-to-token set
+// to the rows' predictions and confidences.
+__global__ __launch_bounds__(256) void threshold_block_kernel(EsParams p) {
+  __shared__ unsigned long long sh_best;
+  __shared__ int32_t sh_changed;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * p.block_size;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    sh_best = 0;
+    sh_changed = 0;
+  }
+  __syncthreads();
+  bool any_gamma = false, any_masked = false;
+  for (int i = tid; i < p.block_size; i += 256) {
+    const int64_t r = r0 + i;
+    const bool masked = p.cur[r] == p.mask_id;
+    const float c = p.conf[r];
+    any_masked |= masked;
+    any_gamma |= masked && c > p.omega_mask;
+    if (masked) {
+      // highest confidence first, then the lowest row: conf is positive, so its
+      // bits order like the value
+      const unsigned long long key = (static_cast<unsigned long long>(__float_as_uint(c)) << 32) |
+                                     (0xffffffffu - static_cast<uint32_t>(i));
+      atomicMax(&sh_best, key);
+    }
+  }
+  any_gamma = __syncthreads_or(any_gamma);
+  any_masked = __syncthreads_or(any_masked);
+  const int forced = (any_masked && !any_gamma) ? static_cast<int>(0xffffffffu - static_cast<uint32_t>(sh_best)) : -1;
+  int changed = 0;
+  for (int i = tid; i < p.block_size; i += 256) {
+    const int64_t r = r0 + i;
+    const int32_t cur = p.cur[r];
+    const int32_t a = p.pred[r];
+    const float c = p.conf[r];
+    uint8_t act = 0;
+    if (cur == p.mask_id) {
+      if (c > p.omega_mask) act = 1;
+      else if (i == forced) act = 2;
+    } else if (a != cur && c >= p.threshold) {
+      act = 3;
+    }
+    p.action[r] = act;
+    p.new_tokens[r] = act ? a : cur;
+    changed += act != 0;
+  }
+  if (changed) atomicAdd(&sh_changed, changed);
+  __syncthreads();
+  if (tid == 0) {
+    p.block_changed[blockIdx.x] = sh_changed != 0;
+    if (p.changed_count && sh_changed) atomicAdd(p.changed_count, sh_changed);
+  }
 }
 
 }  // namespace
@@ -228,16 +335,29 @@ void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chu
   *chunk_len = len;
 }
 
-hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream) {
+template <bool ENT>
+hipError_t launch_rows(const EsParams &p, bool vector_loads, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(p.rows * p.chunks));
   if (vector_loads)
-    hipLaunchKernelGGL(edit_select_kernel<true>, grid, dim3(kT), 0, stream, p);
+    hipLaunchKernelGGL((edit_select_kernel<true, ENT>), grid, dim3(kT), 0, stream, p);
   else
-    hipLaunchKernelGGL(edit_select_kernel<false>, grid, dim3(kT), 0, stream, p);
+    hipLaunchKernelGGL((edit_select_kernel<false, ENT>), grid, dim3(kT), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.chunks == 1) return e;
-  hipLaunchKernelGGL(edit_select_finalize_kernel, dim3(static_cast<unsigned>((p.rows + 255) / 256)), dim3(256), 0,
-                     stream, p);
+  hipLaunchKernelGGL(edit_select_finalize_kernel<ENT>, dim3(static_cast<unsigned>((p.rows + 255) / 256)), dim3(256),
+                     0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream) {
+  return launch_rows<false>(p, vector_loads, stream);
+}
+
+hipError_t launch_threshold_update(const EsParams &p, bool vector_loads, hipStream_t stream) {
+  hipError_t e = p.entropy ? launch_rows<true>(p, vector_loads, stream) : launch_rows<false>(p, vector_loads, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(threshold_block_kernel, dim3(static_cast<unsigned>(p.rows / p.block_size)), dim3(256), 0, stream,
+                     p);
   return hipGetLastError();
 }
 

@@ -51,26 +51,56 @@ constexpr int kEsVecPerThread = 2;   // 16-byte loads per thread per iteration
 
 struct EsPartial {
   float m;        // running max logit
-  float s;        // sum of exp(l - m)
+  float s;        // sum of 2^y, y = (l - m) log2(e)
   int32_t idx;    // lowest index attaining m
-  int32_t pad;
+  float t;        // sum of 2^y * y (entropy accumulator; 0 when not asked for)
 };
 
+// Row reduction (edit selection, or the first step of the threshold update).
 struct EsParams {
   const uint16_t *logits;   // bf16 [rows][ld]
   int64_t rows, vocab, ld;
   int64_t chunk_len;        // elements per chunk, a multiple of 8
   int32_t chunks;           // chunks per row
+  int32_t update;           // 0: edit selection decides; 1: write pred/conf/entropy only
   const int32_t *cur;
-  float threshold;
+  float threshold;          // edit threshold (omega_edit for the update)
   int32_t *new_tokens;
   float *conf;
-  uint8_t *changed;
+  uint8_t *changed;         // edit selection only
   EsPartial *partials;      // [rows][chunks]   (chunks > 1 only)
+  // threshold update
+  int32_t *pred;            // [rows] argmax (workspace)
+  float *entropy;           // [rows] nats, or null
+  int32_t *changed_count;   // zeroed by the row pass, or null
+  uint8_t *action;          // [rows]
+  uint8_t *block_changed;   // [rows / block_size]
+  int32_t mask_id, block_size;
+  float omega_mask;
 };
 
 void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len);
 hipError_t launch_edit_select(const EsParams &p, bool vector_loads, hipStream_t stream);
+hipError_t launch_threshold_update(const EsParams &p, bool vector_loads, hipStream_t stream);
+
+// Tail-entropy scores, start-block choice, refresh flags, KV write-back.
+hipError_t launch_tail_entropy_scores(const float *entropy, int64_t num_blocks, int32_t block_size, int32_t k,
+                                      float *scores, hipStream_t stream);
+hipError_t launch_select_start_block(const float *scores, int32_t batch, int32_t stride, const int32_t *current,
+                                     int32_t k_max, int32_t *start, hipStream_t stream);
+hipError_t launch_refresh_blocks(const uint8_t *changed, int32_t batch, int32_t num_blocks, int32_t mode,
+                                 uint8_t *refresh, hipStream_t stream);
+
+struct KvWriteParams {
+  uint16_t *k_pages, *v_pages;
+  int32_t num_pages, num_kv_heads, head_dim;
+  const int32_t *page_table;
+  int32_t max_pages;
+  const int32_t *start_pos, *lens;
+  int32_t batch, max_len, total_tokens;
+  const uint16_t *k_new, *v_new;   // bf16 [total_tokens][heads][D]
+};
+hipError_t launch_kv_write(const KvWriteParams &p, hipStream_t stream);
 
 
 }  // namespace mbe

@@ -1,0 +1,86 @@
+// Write-back of recomputed K/V into the paged pools, gfx950.
+//
+// Paper, Sec. "Infrastructure Optimization", cache control: the editing pass
+// leaves the cache untouched; afterwards the changed blocks are recomputed
+// under standard attention and their K/V written back.  This kernel is that
+// write: token t of sequence b goes to absolute position start_b + t, i.e.
+// slot (position % 16) of page page_table[b][position / 16].
+//
+// One workgroup per (sequence, page touched, KV head).  K rows are copied as
+// 16-byte chunks.  V is token-minor in the pool ([D][16] per page and head):
+// the workgroup stages its tokens' V rows in LDS, then writes each dim's run
+// of slots, 16 bytes at a time where all 8 slots of a half-row are in range.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace mbe {
+namespace {
+
+__global__ __launch_bounds__(256) void kv_write_kernel(KvWriteParams p) {
+  __shared__ __align__(16) uint16_t vs[kPageSize * 128];   // [slot][D], D <= 128
+  const int b = blockIdx.y;
+  const int g = blockIdx.z;
+  const int D = p.head_dim;
+  const int len = min(max(p.lens[b], 0), p.max_len);
+  if (len == 0) return;
+  const int start = max(p.start_pos[b], 0);
+  const int page_slot = start / kPageSize + static_cast<int>(blockIdx.x);   // page index within the row
+  const int p0 = max(start, page_slot * kPageSize);                          // positions [p0, p1) on this page
+  const int p1 = min(start + len, (page_slot + 1) * kPageSize);
+  if (p0 >= p1) return;
+  // first row of sequence b
+  int64_t row0 = 0;
+  for (int j = 0; j < b; ++j) row0 += min(max(p.lens[j], 0), p.max_len);
+  const int slot_row = min(page_slot, p.max_pages - 1);
+  const int64_t page = min(max(p.page_table[static_cast<int64_t>(b) * p.max_pages + slot_row], 0), p.num_pages - 1);
+  const int64_t page_base = (page * p.num_kv_heads + g) * static_cast<int64_t>(kPageSize) * D;   // elements
+  const int chunks = D / 8;
+  const int n = p1 - p0;
+  // K: [slot][D], a 16-byte chunk per thread
+  for (int i = threadIdx.x; i < n * chunks; i += 256) {
+    const int tok = i / chunks, c = i % chunks;
+    const int64_t row = row0 + (p0 - start) + tok;
+    if (row >= p.total_tokens) continue;
+    const uint4 w = *reinterpret_cast<const uint4 *>(p.k_new + (row * p.num_kv_heads + g) * D + c * 8);
+    *reinterpret_cast<uint4 *>(p.k_pages + page_base + ((p0 + tok) % kPageSize) * D + c * 8) = w;
+  }
+  // V: stage [slot][D] in LDS, then write [D][slot]
+  for (int i = threadIdx.x; i < n * chunks; i += 256) {
+    const int tok = i / chunks, c = i % chunks;
+    const int64_t row = row0 + (p0 - start) + tok;
+    uint4 w = make_uint4(0, 0, 0, 0);
+    if (row < p.total_tokens) w = *reinterpret_cast<const uint4 *>(p.v_new + (row * p.num_kv_heads + g) * D + c * 8);
+    *reinterpret_cast<uint4 *>(vs + ((p0 + tok) % kPageSize) * D + c * 8) = w;
+  }
+  __syncthreads();
+  const int s0 = p0 % kPageSize, s1 = s0 + n;       // slots [s0, s1) on this page
+  for (int i = threadIdx.x; i < D * 2; i += 256) {   // (dim, half of 8 slots)
+    const int d = i >> 1, h = i & 1;
+    const int a = h * 8, e = a + 8;
+    uint16_t *dst = p.v_pages + page_base + static_cast<int64_t>(d) * kPageSize + a;
+    if (s0 <= a && e <= s1) {
+      uint4 w;
+      uint32_t *u = reinterpret_cast<uint32_t *>(&w);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        u[k] = static_cast<uint32_t>(vs[(a + 2 * k) * D + d]) | (static_cast<uint32_t>(vs[(a + 2 * k + 1) * D + d]) << 16);
+      *reinterpret_cast<uint4 *>(dst) = w;
+    } else {
+      for (int s = max(a, s0); s < min(e, s1); ++s) dst[s - a] = vs[s * D + d];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_write(const KvWriteParams &p, hipStream_t stream) {
+  // pages a sequence's range can touch: ceil(max_len / 16) + 1 (an unaligned start)
+  const unsigned pages = static_cast<unsigned>((p.max_len + kPageSize - 1) / kPageSize + 1);
+  hipLaunchKernelGGL(kv_write_kernel, dim3(pages, static_cast<unsigned>(p.batch), static_cast<unsigned>(p.num_kv_heads)),
+                     dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace mbe

@@ -27,7 +27,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert len(names) == 7, names
+    assert len(names) == 13, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(mbe.EXPORTS)
@@ -146,3 +146,97 @@ def test_missing_library_fails_loudly(tmp_path):
             m.load(str(tmp_path / "nope.so"))
     finally:
         importlib.reload(mbe)
+
+
+def _vp(x):
+    return None if x is None else ctypes.c_void_p(x)
+
+
+@pytest.mark.parametrize("args,status,text", [
+    (dict(rows=-1), 2, "negative"),
+    (dict(block_size=0), 2, "block_size"),
+    (dict(rows=30, block_size=32), 2, "multiple of block_size"),
+    (dict(row_stride=100, vocab=128), 2, "row_stride"),
+    (dict(omega_mask=float("nan")), 6, "NaN"),
+    (dict(omega_edit=float("nan")), 6, "NaN"),
+    (dict(action=None), 1, "non-NULL"),
+    (dict(block_changed=None), 1, "non-NULL"),
+    (dict(ws=None), 4, "workspace"),
+    (dict(wsb=16), 4, "workspace"),
+    (dict(ws=272), 4, "aligned"),
+])
+def test_threshold_update_validation(lib, args, status, text):
+    a = dict(logits=16, rows=64, vocab=128, row_stride=128, cur=16, mask_id=127, block_size=32, omega_mask=0.5,
+             omega_edit=0.0, new=16, conf=16, action=16, block_changed=16, count=None, entropy=None, ws=256,
+             wsb=1 << 20)
+    a.update(args)
+    st = lib.mbe_threshold_update(_vp(a["logits"]), a["rows"], a["vocab"], a["row_stride"], _vp(a["cur"]),
+                                  a["mask_id"], a["block_size"], ctypes.c_float(a["omega_mask"]),
+                                  ctypes.c_float(a["omega_edit"]), _vp(a["new"]), _vp(a["conf"]), _vp(a["action"]),
+                                  _vp(a["block_changed"]), _vp(a["count"]), _vp(a["entropy"]), _vp(a["ws"]),
+                                  a["wsb"], None)
+    assert st == status and text in lib.mbe_last_error().decode(), lib.mbe_last_error()
+
+
+def test_threshold_update_workspace_and_empty(lib):
+    assert lib.mbe_threshold_update_workspace_size(-1, 10) == ctypes.c_size_t(-1).value
+    assert lib.mbe_threshold_update_workspace_size(0, 10) == 0
+    n = lib.mbe_threshold_update_workspace_size(8192, 131072)
+    assert n >= 8192 * 4 and n % 256 == 0
+    assert lib.mbe_threshold_update_workspace_size(64, 131072) > lib.mbe_edit_select_workspace_size(64, 131072)
+    assert lib.mbe_threshold_update(None, 0, 128, 128, None, 0, 32, ctypes.c_float(0.5), ctypes.c_float(0.0),
+                                    None, None, None, None, None, None, None, 0, None) == 0
+
+
+@pytest.mark.parametrize("args,status,text", [
+    (dict(num_blocks=-1), 2, "num_blocks"),
+    (dict(block_size=0), 3, "block_size"),
+    (dict(block_size=2048), 3, "block_size"),
+    (dict(rho=0.0), 6, "rho"),
+    (dict(rho=1.5), 6, "rho"),
+    (dict(rho=float("nan")), 6, "rho"),
+    (dict(entropy=None), 1, "non-NULL"),
+])
+def test_tail_entropy_validation(lib, args, status, text):
+    a = dict(entropy=16, num_blocks=4, block_size=32, rho=0.25, scores=16)
+    a.update(args)
+    st = lib.mbe_tail_entropy_scores(_vp(a["entropy"]), a["num_blocks"], a["block_size"], ctypes.c_float(a["rho"]),
+                                     _vp(a["scores"]), None)
+    assert st == status and text in lib.mbe_last_error().decode()
+
+
+@pytest.mark.parametrize("args,status,text", [
+    (dict(batch=-1), 2, "batch"),
+    (dict(k_max=0), 2, "k_max"),
+    (dict(current=None), 1, "non-NULL"),
+])
+def test_select_start_validation(lib, args, status, text):
+    a = dict(scores=16, batch=4, stride=8, current=16, k_max=4, start=16)
+    a.update(args)
+    st = lib.mbe_select_start_block(_vp(a["scores"]), a["batch"], a["stride"], _vp(a["current"]), a["k_max"],
+                                    _vp(a["start"]), None)
+    assert st == status and text in lib.mbe_last_error().decode()
+
+
+@pytest.mark.parametrize("args,status,text", [
+    (dict(head_dim=96), 3, "head_dim"),
+    (dict(batch=70000), 2, "batch"),
+    (dict(max_len=-1), 2, "negative"),
+    (dict(k_new=None), 1, "non-NULL"),
+    (dict(v_pages=24), 2, "aligned"),
+    (dict(num_pages=0), 2, "empty"),
+])
+def test_kv_write_validation(lib, args, status, text):
+    a = dict(k_pages=16, v_pages=32, num_pages=10, heads=4, head_dim=128, pt=16, max_pages=8, start=16, lens=16,
+             batch=2, max_len=64, total=96, k_new=16, v_new=16)
+    a.update(args)
+    st = lib.mbe_kv_write(_vp(a["k_pages"]), _vp(a["v_pages"]), a["num_pages"], a["heads"], a["head_dim"],
+                          _vp(a["pt"]), a["max_pages"], _vp(a["start"]), _vp(a["lens"]), a["batch"], a["max_len"],
+                          a["total"], _vp(a["k_new"]), _vp(a["v_new"]), None)
+    assert st == status and text in lib.mbe_last_error().decode()
+
+
+def test_refresh_validation(lib):
+    assert lib.mbe_refresh_blocks(_vp(16), 2, 4, 2, _vp(16), None) == 3
+    assert lib.mbe_refresh_blocks(None, 2, 4, 0, _vp(16), None) == 1
+    assert lib.mbe_refresh_blocks(None, 0, 4, 0, None, None) == 0
