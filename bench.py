@@ -104,11 +104,16 @@ def _counter_rows(path):
 
 
 _KERNELS = {"window_attention_kernel": "window_attention", "window_attention_merge_kernel": "window_attention_merge",
-            "edit_select_kernel": "edit_select", "edit_select_finalize_kernel": "edit_select_finalize"}
+            "edit_select_kernel": "edit_select", "edit_select_finalize_kernel": "edit_select_finalize",
+            "threshold_block_kernel": "threshold_update_blocks", "kv_write_kernel": "kv_write",
+            "tail_entropy_kernel": "tail_entropy_scores", "select_start_kernel": "select_start_block",
+            "refresh_kernel": "refresh_blocks"}
 
 
 def _kernel_key(name):
     # "window_attention_kernel<" also prefixes the merge kernel's name: match on the full token
+    if "edit_select_kernel<" in name and name.split("edit_select_kernel<")[1].startswith(("true, true", "false, true")):
+        return "threshold_update_rows"      # the row pass with the entropy accumulator
     for k in sorted(_KERNELS, key=len, reverse=True):
         if k + "<" in name or k + "(" in name:
             return _KERNELS[k]
@@ -201,6 +206,11 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
                   "| kernel | rocprofv3 trace average (us) | bench.py event average (us) |", "|---|---|---|"]
         ev = {"window_attention": line["attention"]["ms"] * 1e3,
               "edit_select": (line.get("edit_select") or {}).get("ms", 0) * 1e3}
+        nxt = line.get("next_rows") or {}
+        for key, name in (("kv_write", "kv_write"), ("tail_entropy_scores", "tail_entropy_scores"),
+                          ("select_start_block", "select_start_block")):
+            if key in nxt:
+                ev[name] = nxt[key]["ms"] * 1e3
         by = {}
         for r in sorted(trace, key=lambda r: int(r["Start_Timestamp"])):
             k = _kernel_key(r["Kernel_Name"])
@@ -209,7 +219,10 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
         for k, d in sorted(by.items()):
             d = d[-steps:]
             lines.append(f"| {k} | {sum(d) / len(d):.2f} | {ev[k]:.2f} |" if k in ev else
-                         f"| {k} | {sum(d) / len(d):.2f} | (inside the attention call) |")
+                         f"| {k} | {sum(d) / len(d):.2f} | (part of a call timed as a whole) |")
+        if nxt:
+            lines += ["", f"threshold_update (row pass with entropy + block pass) timed as one call: "
+                          f"{nxt['threshold_update']['ms'] * 1e3:.2f} us by HIP events."]
     if line:
         lines += ["", "JSON line printed by the profiled run:", "", "```", json.dumps(line), "```"]
     with open(out_path, "w") as f:
