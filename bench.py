@@ -281,7 +281,40 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
     jcur = torch.full((attn_case.batch,), nb, dtype=torch.int32, device=dev)
     t_tail = _time_events(lambda: mbe.tail_entropy_scores(ent, B, 0.25, out=scores), steps)
     t_sel = _time_events(lambda: mbe.select_start_block(sc2, jcur, 4), steps)
+    # one editing pass (attention + threshold update with entropy) at small
+    # shapes, launched eagerly through the binding vs replayed from the
+    # multi-shape graph pool
+    from paper_2607_22663_amd.graphs import EditPassGraphs
+    pool_rows = {}
+    max_p = int(attn_case.prefix_lens.max())
+    pool = EditPassGraphs(k_pages=c.k_pages, v_pages=c.v_pages, max_batch=8, max_window=64, block_size=B,
+                          num_q_heads=attn_case.num_q_heads, max_pages_per_seq=c.page_table.shape[1],
+                          max_prefix_len=max_p, vocab=V, mask_id=V - 1)
+    for nb, win in ((1, 32), (1, 64), (8, 64)):
+        n = nb * win
+        pool.capture(nb, win)
+        inp = pool.inputs(nb, win)
+        inp["q"].copy_(c.q[:n])
+        inp["page_table"].copy_(c.page_table[:nb])
+        inp["prefix_lens"].copy_(P[:nb])
+        inp["logits"].copy_(logits[:n])
+        inp["cur_tokens"].copy_(cur_m[:n])
+        qv, ptv, pv = c.q[:n], c.page_table[:nb].contiguous(), P[:nb]
+        wv = torch.full((nb,), win, dtype=torch.int32, device=dev)
+        lv, cv = logits[:n], cur_m[:n]
+        o_att = torch.empty_like(qv)
+        o_upd = mbe.threshold_update(lv, cv, V - 1, B, 0.5, 0.0, with_entropy=True)
+
+        def eager():
+            mbe.window_attention(qv, c.k_pages, c.v_pages, ptv, pv, wv, B, out=o_att, max_prefix_len=max_p,
+                                 max_window_len=win)
+            mbe.threshold_update(lv, cv, V - 1, B, 0.5, 0.0, with_entropy=True, out=o_upd)
+        t_e = _time_events(eager, steps)
+        t_g = _time_events(lambda: pool.replay(nb, win), steps)
+        pool_rows[f"{nb}x{win}"] = {"eager_ms": round(t_e * 1e3, 4), "graph_ms": round(t_g * 1e3, 4)}
+    del pool
     return {
+        "graph_pool_edit_pass": pool_rows,
         "threshold_update": {"ms": round(t_upd * 1e3, 4), "rows": R, "vocab": V, "block": B,
                              "with_entropy": True, "algorithmic_mb": round(upd_bytes / 1e6, 1),
                              "gbs": round(upd_bytes / t_upd / 1e9, 1),

@@ -145,6 +145,34 @@ def _workspace(kind: str, device: torch.device, nbytes: int) -> Optional[torch.T
     return ws
 
 
+def _own_workspace(ws: torch.Tensor, need: int) -> Optional[torch.Tensor]:
+    if need == 0:
+        return None
+    if ws.dtype != torch.uint8 or not ws.is_cuda or ws.numel() < need:
+        raise ValueError(f"workspace must be a uint8 device tensor of at least {need} bytes")
+    return ws
+
+
+def workspace_bytes_threshold_update(rows, vocab):
+    n = load().mbe_threshold_update_workspace_size(int(rows), int(vocab))
+    return 0 if n == ctypes.c_size_t(-1).value else n
+
+
+def workspace_bytes_window_attention(q, k_pages, page_table, batch, block_size, *, max_prefix_len,
+                                     max_window_len, mask_mode="bidir", kv_split_tokens=0):
+    """Workspace bytes of a window_attention call planned from bounds only
+    (no host lengths), as a captured graph replays it."""
+    lib = load()
+    kv = PagedKV(None, None, k_pages.shape[0], k_pages.shape[2], k_pages.shape[1], k_pages.shape[3])
+    opts = AttnOpts(int(batch), q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len), int(max_window_len),
+                    MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode), 0.0,
+                    int(kv_split_tokens), None, None, None, 0, None)
+    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+    if n == ctypes.c_size_t(-1).value:
+        raise ValueError("invalid attention shapes")
+    return n
+
+
 def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
@@ -186,7 +214,8 @@ def _host_i32(x, batch, name):
 
 def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size, *,
                      out=None, mask_mode="bidir", softmax_scale=None, max_prefix_len=None,
-                     max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None):
+                     max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None,
+                     workspace=None):
     """MBE editing-window attention (paper, Sec. "Training-Free MBE Decoding",
     Eq. (4)).  Layouts as in include/mbe.h.
 
@@ -194,7 +223,9 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     host_window_lens are optional host copies of the lengths (they let the
     library size splits from the total work and start long sequences first).
     When neither bounds nor host lengths are given, the lengths are copied
-    from the device (a synchronisation)."""
+    from the device (a synchronisation).  workspace: an optional caller-owned
+    uint8 device tensor used instead of the module's shared one (as a
+    captured graph needs)."""
     lib = load()
     kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
     _need(window_lens, "window_lens", torch.int32, q.device, 1)
@@ -217,7 +248,7 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     if need == ctypes.c_size_t(-1).value:
         _check("mbe_window_attention", lib.mbe_window_attention(
             None, ctypes.byref(kv), None, None, None, int(block_size), None, ctypes.byref(opts)))
-    ws = _workspace("attn", q.device, need)
+    ws = _workspace("attn", q.device, need) if workspace is None else _own_workspace(workspace, need)
     opts.workspace = _ptr(ws)
     opts.workspace_bytes = need
     _check("mbe_window_attention", lib.mbe_window_attention(
@@ -285,7 +316,7 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
 
 
 def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_edit, *, vocab=None,
-                     with_entropy=False, out=None):
+                     with_entropy=False, out=None, workspace=None):
     """Full threshold update (paper, Eq. (1) with force-unmask).  Rows form
     blocks of block_size consecutive rows.  Returns a dict of device tensors:
     new_tokens int32, conf float32, action uint8 (ACTIONS), block_changed
@@ -311,7 +342,8 @@ def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_
         if with_entropy:
             out["entropy"] = torch.empty(rows, dtype=torch.float32, device=dev)
     need = lib.mbe_threshold_update_workspace_size(rows, v)
-    ws = _workspace("update", dev, need if need != ctypes.c_size_t(-1).value else 0)
+    need = need if need != ctypes.c_size_t(-1).value else 0
+    ws = _workspace("update", dev, need) if workspace is None else _own_workspace(workspace, need)
     _check("mbe_threshold_update", lib.mbe_threshold_update(
         _ptr(logits), rows, v, ld, _ptr(cur_tokens), int(mask_id), int(block_size), ctypes.c_float(omega_mask),
         ctypes.c_float(omega_edit), _ptr(out["new_tokens"]), _ptr(out["conf"]), _ptr(out["action"]),
