@@ -96,8 +96,7 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   // Host copies of the lengths, when given, refine the plan.
   const bool host = o->host_prefix_lens && (fixed_window_of(o, window_bound) >= 0 || o->host_window_lens) &&
                     o->batch > 0 && o->batch <= mbe::kMaxOrderedSeqs;
-  std::vector<int64_t> n_seq;
-  int64_t work = 0;    // sum over work units (sequence, KV head, query tile) of the keys they read
+  std::vector<int64_t> n_seq;   // keys each sequence's units read
   if (host) {
     n_seq.resize(o->batch);
     for (int b = 0; b < o->batch; ++b) {
@@ -107,19 +106,44 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
         return fail(MBE_ERR_BAD_SHAPE, "host lengths of sequence %d (%lld, %lld) exceed the bounds", b,
                     static_cast<long long>(P), static_cast<long long>(W));
       n_seq[b] = W > 0 ? P + W : 0;
-      const int64_t qt = (pl->group * W + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile;
-      work += kv->num_kv_heads * qt * n_seq[b];
     }
-  } else {
-    work = base_units * max_kv;
   }
 
   int64_t chunk = o->kv_split_tokens;
   if (chunk == 0) {
-    // Keys per split so that the work fills the CUs once: long sequences of a
-    // small batch are split, a large batch is not (each split costs a
-    // pipeline fill and a merge of partial results).
-    chunk = std::max<int64_t>(kMinChunk, (work + kConcurrentUnits - 1) / kConcurrentUnits);
+    // Work units (sequence, KV head, query tile, split) with splits of c keys.
+    auto units = [&](int64_t c) {
+      int64_t u = 0;
+      if (host) {
+        for (int b = 0; b < o->batch; ++b) {
+          if (n_seq[b] == 0) continue;
+          const int64_t W = fixed_window_of(o, window_bound) >= 0 ? fixed_window_of(o, window_bound) : o->host_window_lens[b];
+          const int64_t qt = (pl->group * W + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile;
+          u += kv->num_kv_heads * qt * ((n_seq[b] + c - 1) / c);
+        }
+      } else {
+        u = base_units * ((max_kv + c - 1) / c);
+      }
+      return u;
+    };
+    const int64_t c_max = std::max<int64_t>(kMinChunk, (max_kv + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
+    if (units(c_max) > kConcurrentUnits) {
+      // More units than CUs already: no split (each split adds a pipeline fill
+      // and a merge of partial results, and the longest-first order balances
+      // the units of a large batch).
+      chunk = c_max;
+    } else {
+      // Splits as short as possible while every unit still starts in the first
+      // round on the 256 CUs: the smallest multiple of 64 keys whose unit count
+      // fits (the count only falls as the split grows).
+      int64_t lo = std::max<int64_t>(kMinChunk / mbe::kKeyTile, 1), hi = c_max / mbe::kKeyTile;
+      while (lo < hi) {
+        const int64_t mid = (lo + hi) / 2;
+        if (units(mid * mbe::kKeyTile) <= kConcurrentUnits) hi = mid;
+        else lo = mid + 1;
+      }
+      chunk = lo * mbe::kKeyTile;
+    }
   }
   chunk = std::max<int64_t>(mbe::kKeyTile, (chunk + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
   pl->kv_chunk = static_cast<int32_t>(std::min<int64_t>(chunk, 1LL << 30));
