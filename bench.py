@@ -172,6 +172,46 @@ def summarize_pmc(dirs, workload):
     print("\n".join(lines))
 
 
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES",
+                 "GRBM_GUI_ACTIVE")
+
+
+def summarize_mfma(pmc_dir, bench_stdout, out_path, command, workload):
+    """Markdown summary of one rocprofv3 --pmc pass of MFMA counters over the
+    attention kernel: the bf16 MFMA work the hardware counted (MOPS, units of
+    512 flops) against the algorithmic FLOPs, and the MFMA-busy share."""
+    rows = [r for r in _counter_rows(pmc_dir) if _kernel_key(r["Kernel_Name"]) == "window_attention"]
+    per = {}
+    for r in rows:
+        per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    avg = {k: sum(v) / len(v) for k, v in per.items()}
+    line = None
+    with open(bench_stdout) as f:
+        for ln in f:
+            if ln.startswith("{"):
+                line = json.loads(ln)
+    gflop = line["attention"]["gflop"] if line else float("nan")
+    counted = avg.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512 / 1e9
+    mfma_insts = avg.get("SQ_INSTS_MFMA", 0.0)
+    lines = ["# window attention: MFMA counters", "", f"Workload {workload}, one rocprofv3 --pmc pass, average per "
+             f"dispatch over {len(rows) // max(1, len(per))} dispatches.", "", "Command:", "", "```", command, "```", "",
+             "| counter | value per dispatch |", "|---|---|"]
+    for k in MFMA_COUNTERS:
+        if k in avg:
+            lines.append(f"| {k} | {avg[k]:.4g} |")
+    lines += ["", f"- bf16 MFMA work counted: {counted:.1f} GFLOP (MOPS x 512) against {gflop:.1f} GFLOP algorithmic "
+              f"(ratio {counted / gflop:.4f}; the extra is the reference block, whose scores are formed twice).",
+              f"- MFMA instructions: {mfma_insts:.4g} (32x32x16 bf16, 32768 flops each: "
+              f"{mfma_insts * 32768 / 1e9:.1f} GFLOP)."]
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and "GRBM_GUI_ACTIVE" in avg:
+        busy = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * 256 * avg["GRBM_GUI_ACTIVE"] / 8)
+        lines.append(f"- MFMA busy share: {100 * busy:.1f}% = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x 256 CUs x "
+                     "GRBM_GUI_ACTIVE / 8), reading GRBM_GUI_ACTIVE as summed over the 8 XCDs.")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_stats(stats_dir, bench_stdout, out_path, command):
     """Writes a short markdown summary of a rocprofv3 --kernel-trace --stats run
     of this script: rocprofv3's per-kernel statistics, the average over the
@@ -354,10 +394,20 @@ def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_s
     edit_rate = edit_bytes(er, edit_case.logits.shape[1]) / t_edit   # byte/s
     t_step = flops_total / attn_rate + edit_bytes_total / edit_rate
     sol = flops_total / (PEAK_BF16_TFLOPS * 1e12) + edit_bytes_total / (PEAK_HBM_GBS * 1e9)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {
         "value": 100.0 * sol / t_step,
         "unit": "% of MI355X peak (speed-of-light step time / oracle step time)",
         "cores": int(cores),
+        "cpu": model,
         "kind": "oracle",
         "sample": (f"fp64 numpy oracle: window attention of the first {nb} of {c.batch} sequences "
                    f"({sub_flops / 1e9:.1f} GFLOP, {t_attn:.1f} s) and edit selection of the first {er} "
@@ -379,6 +429,7 @@ def main():
     ap.add_argument("--kv-split-tokens", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
+    ap.add_argument("--no-flush", action="store_true", help="do not flush the infinity cache before each step")
     ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
@@ -386,12 +437,17 @@ def main():
                          "WRITE_SIZE, optionally the TCC_EA0_RDREQ_* request-size pass) and exit")
     ap.add_argument("--summarize-stats", nargs=4, metavar=("STATS_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
                     help="write a markdown summary of a rocprofv3 --kernel-trace --stats run and exit")
+    ap.add_argument("--summarize-mfma", nargs=4, metavar=("PMC_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --pmc pass of MFMA counters and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc, args.workload)
         return
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma, args.workload)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -457,9 +513,14 @@ def main():
     n = args.steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
     stream = torch.cuda.current_stream(dev)
+    # Before every timed step a 512 MiB buffer is written, outside the events,
+    # so that no input of the step is served from the 256 MB infinity cache.
+    flush = None if args.no_flush else torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     for i in range(n):
+        if flush is not None:
+            flush.fill_(i & 0xFF)
         ev[i][0].record(stream)
         attention()
         ev[i][1].record(stream)
@@ -468,14 +529,19 @@ def main():
         ev[i][2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
-    t_attn = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) / 1e3
-    t_edit = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) / 1e3 if edit_case is not None else 0.0
+    del flush
+    d_attn = np.array([e[0].elapsed_time(e[1]) for e in ev]) / 1e3
+    d_edit = np.array([e[1].elapsed_time(e[2]) for e in ev]) / 1e3
+    t_attn = float(np.mean(d_attn))
+    t_edit = float(np.mean(d_edit)) if edit_case is not None else 0.0
     t_step = float(np.mean([e[0].elapsed_time(e[2]) for e in ev])) / 1e3
 
     flops, attn_bytes = attention_work(attn_case)
     e_bytes = edit_bytes(R, V) if edit_case is not None else 0
     sol = flops / (PEAK_BF16_TFLOPS * 1e12) + e_bytes / (PEAK_HBM_GBS * 1e9)
     attn_tflops = flops / t_attn / 1e12
+    # the attention roofline of this workload: min(MFMA peak, intensity x HBM peak)
+    attn_roof = min(PEAK_BF16_TFLOPS, flops / attn_bytes * PEAK_HBM_GBS / 1e3)
     edit_gbs = e_bytes / t_edit / 1e9 if edit_case is not None else None
 
     traffic = measured_traffic("window_attention", args.workload)
@@ -503,10 +569,16 @@ def main():
             "edit_rows": R if edit_case is not None else 0, "vocab": V if edit_case is not None else 0,
             "kv_split_tokens": args.kv_split_tokens,
         },
-        "attention": {"ms": round(t_attn * 1e3, 4), "tflops": round(attn_tflops, 2),
+        "attention": {"ms": round(t_attn * 1e3, 4), "ms_median": round(float(np.median(d_attn)) * 1e3, 4),
+                      "ms_min": round(float(np.min(d_attn)) * 1e3, 4), "tflops": round(attn_tflops, 2),
                       "pct_mfma_peak": round(100 * attn_tflops / PEAK_BF16_TFLOPS, 2),
-                      "gflop": round(flops / 1e9, 2), "algorithmic_mb": round(attn_bytes / 1e6, 1)},
-        "edit_select": ({"ms": round(t_edit * 1e3, 4), "gbs": round(edit_gbs, 1),
+                      "gflop": round(flops / 1e9, 2), "algorithmic_mb": round(attn_bytes / 1e6, 1),
+                      "flop_per_byte": round(flops / attn_bytes, 1),
+                      "roofline_tflops": round(attn_roof, 1),
+                      "pct_of_roofline": round(100 * attn_tflops / attn_roof, 2)},
+        "cache": "cold: 512 MiB written before every step" if not args.no_flush else "warm (no flush)",
+        "edit_select": ({"ms": round(t_edit * 1e3, 4), "ms_median": round(float(np.median(d_edit)) * 1e3, 4),
+                         "ms_min": round(float(np.min(d_edit)) * 1e3, 4), "gbs": round(edit_gbs, 1),
                          "pct_hbm_peak": round(100 * edit_gbs / PEAK_HBM_GBS, 2),
                          "algorithmic_mb": round(e_bytes / 1e6, 1),
                          "traffic": measured_traffic("edit_select", args.workload)}
