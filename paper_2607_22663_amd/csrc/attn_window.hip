@@ -196,7 +196,11 @@ __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
   }
 }
 
-template <int D, int MODE>
+// KS = 1: the four waves own 64 rows each.  KS = 2 (at most 128 rows per
+// sequence and KV head): waves w and w + 2 own the same 64 rows and split the
+// keys, wave w taking the first and wave w + 2 the second 32-key block of
+// every tile; their partial results are added at the end.
+template <int D, int MODE, int KS>
 __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // four K/V tile buffers (separate objects, so the compiler can tell which
   // in-flight direct loads a read depends on), three tiles in flight
@@ -219,7 +223,6 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int rank = static_cast<int>(rg / p.num_kv_heads);
   const int g = static_cast<int>(rg % p.num_kv_heads);
   const int b = rank < p.seq_order_n ? p.seq_order[rank] : rank;
-  const int bg = b * p.num_kv_heads + g;
 
   const int G = p.group;
   // lengths are clamped to the host-validated bounds, so a wrong device value
@@ -240,6 +243,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int wave = tid >> 6;
   const int c = lane & 31;       // query column of this lane
   const int h = lane >> 5;       // which half of the 32x32 MFMA layout
+  const int wrow = KS == 2 ? (wave & 1) : wave;   // 64-row slice of this wave
+  const int kown = KS == 2 ? (wave >> 1) : 0;     // 32-key block of each tile (KS = 2)
 
   // first query row of sequence b
   int cu = 0;
@@ -257,7 +262,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   int64_t qoff[2];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    const int r = row0 + wave * kRowsPerWave + qb * 32 + c;
+    const int r = row0 + wrow * kRowsPerWave + qb * 32 + c;
     valid[qb] = r < M && cu + r / G < p.total_q;
     const int i = valid[qb] ? r / G : 0;
     const int hq = g * G + (valid[qb] ? r % G : 0);
@@ -274,10 +279,6 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     kend = min(ke, P + (i_last / p.block_size + 1) * p.block_size);
   }
   const int ntiles = kend > kb ? (kend - kb + kKeyTile - 1) / kKeyTile : 0;
-  // smallest limit over the wave: tiles ending at or below it need no mask
-  int wmin = min(lim[0], lim[1]);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) wmin = min(wmin, __shfl_xor(wmin, o));
 
   // ---- Q^T operands in registers: lane (c, h) holds dims 16kk + 8h .. +7
   constexpr int KK = D / 16;
@@ -440,18 +441,27 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   auto compute = [&](const char *buf, int t, auto masked) {
     const int key0 = kb + t * kKeyTile;
-    f32x16 s0[2], s1[2];
-    qk_block(buf, 0, s0);
-    qk_block(buf, 1, s1);
-    if constexpr (decltype(masked)::value) {
-      mask_block(key0, s0);
-      mask_block(key0 + 32, s1);
+    if constexpr (KS == 2) {
+      f32x16 s0[2];
+      qk_block(buf, kown, s0);
+      if constexpr (decltype(masked)::value) mask_block(key0 + 32 * kown, s0);
+      bf16x8 va[2][DB];
+      read_v(buf, kown, va);
+      softmax_pv(va, s0);
+    } else {
+      f32x16 s0[2], s1[2];
+      qk_block(buf, 0, s0);
+      qk_block(buf, 1, s1);
+      if constexpr (decltype(masked)::value) {
+        mask_block(key0, s0);
+        mask_block(key0 + 32, s1);
+      }
+      bf16x8 va[2][DB];
+      read_v(buf, 0, va);
+      softmax_pv(va, s0);
+      read_v(buf, 1, va);
+      softmax_pv(va, s1);
     }
-    bf16x8 va[2][DB];
-    read_v(buf, 0, va);
-    softmax_pv(va, s0);
-    read_v(buf, 1, va);
-    softmax_pv(va, s1);
   };
   // one tile through dynamically chosen buffers (remainder, masked tiles)
   auto generic_step = [&](int t, bool masked) {
@@ -533,6 +543,35 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       bad |= valid[qb] && !(lt <= kSumLimit);
     }
     if (!__syncthreads_or(bad)) break;
+  }
+
+  if constexpr (KS == 2) {
+    // waves 2 and 3 hand their partial O and row sums (same reference) to
+    // waves 0 and 1 through the tile buffers, which no wave reads any more:
+    // wave 2 + j writes its O to buffer j and its sums to buffer 2
+    static_assert(2 * DB * 16 * 64 * 4 <= Tile<D>::kBufBytes, "partial O fits one buffer");
+    float *xo = reinterpret_cast<float *>(wrow == 0 ? lds0 : lds1);
+    float *xl = reinterpret_cast<float *>(lds2) + wrow * 2 * 64;
+    if (kown == 1) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) xo[((qb * DB + db) * 16 + v) * 64 + lane] = acc_o[qb][db][v];
+        xl[qb * 64 + lane] = l_run[qb];
+      }
+    }
+    lds_barrier();
+    if (kown == 1) return;      // no barrier follows
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc_o[qb][db][v] += xo[((qb * DB + db) * 16 + v) * 64 + lane];
+      l_run[qb] += xl[qb * 64 + lane];
+    }
   }
 
   // ---- epilogue
@@ -636,8 +675,12 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
 template <int D, int MODE>
 hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
   const int64_t grid = p.slots_per_xcd * kXcds;
-  hipLaunchKernelGGL((window_attention_kernel<D, MODE>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
-                     stream, p);
+  if (p.key_split == 2)
+    hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
+                       stream, p);
+  else
+    hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
+                       stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits == 1) return e;
   const int64_t items = static_cast<int64_t>(p.max_window) * p.num_q_heads * (D / 4);

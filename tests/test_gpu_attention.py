@@ -65,6 +65,75 @@ def test_ragged_batch_with_poisoned_tails(gpu, D, mode):
         assert_attn_close(out, oracle_case(case, mode), f"ragged D={D} {mode} split={split}")
 
 
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_key_split_waves_ragged(gpu, D, mode):
+    """At most 128 rows per (sequence, KV head) (here 2 query heads per KV head,
+    windows up to 64): pairs of waves split every key tile and add their
+    partial results.  Ragged prefixes, an empty window, poisoned page tails."""
+    spec = synth.AttnSpec(4, 32, 1, ("fixed", 0), 8, 4, D)
+    case = synth.make_attention_case(spec, 31, prefix_lens=[0, 45, 1300, 211],
+                                     window_lens=[64, 32, 64, 0], extra_pages=2,
+                                     tail_fill=float("nan"))
+    say(f"  D={D} mode={mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
+    for split in (0, 64, 320):
+        out = run_case(gpu, case, mode, kv_split_tokens=split)
+        assert_attn_close(out, oracle_case(case, mode), f"key split D={D} {mode} split={split}")
+
+
+def test_key_split_waves_sharp_scores(gpu):
+    """Single-block windows with 16 query / 4 KV heads (128 rows: the key-split
+    path) and Q scaled by 8: scores spread over tens of log2 units, so later
+    keys exceed the first block's maximum (the fixed softmax reference)."""
+    spec = synth.AttnSpec(3, 32, 1, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 41, prefix_lens=[2000, 64, 777], q_scale=8.0)
+    for split in (0, 256):
+        out = run_case(gpu, case, "bidir", kv_split_tokens=split)
+        assert_attn_close(out, oracle_case(case), f"key split sharp split={split}")
+
+
+def _plant_hot_keys(case, seed, q_gain=6.0, hot_per_seq=5):
+    """Q rows = q_gain * s + N(0,1) for one sign vector s per KV head, and a few
+    keys past the first 64 of each sequence set to s * U(0.9, 1): their scores
+    lie ~100 log2 units above the first 32-key block's, so the fixed-reference
+    row sums overflow and the kernel must take its exact rerun."""
+    rng = np.random.default_rng(seed)
+    Hq, Hkv, D = case.num_q_heads, case.num_kv_heads, case.head_dim
+    G = Hq // Hkv
+    sgn = rng.choice([-1.0, 1.0], size=(Hkv, D))
+    q = case.q.float().numpy()
+    noise = rng.standard_normal(q.shape)
+    q = q_gain * np.repeat(sgn, G, axis=0)[None, :, :] + noise
+    k = case.k_pages.float().numpy().copy()
+    pt = case.page_table.numpy()
+    P, W = case.prefix_lens.numpy(), case.window_lens.numpy()
+    for b in range(case.batch):
+        n = int(P[b] + W[b])
+        if n <= 64:
+            continue
+        for t in rng.choice(np.arange(64, n), size=min(hot_per_seq, n - 64), replace=False):
+            page, slot = pt[b, t // 16], t % 16
+            k[page, :, slot, :] = sgn * rng.uniform(0.9, 1.0, size=(Hkv, D))
+    case.q = torch.from_numpy(q).to(torch.bfloat16)
+    case.k_pages = torch.from_numpy(k).to(torch.bfloat16)
+    return case
+
+
+@pytest.mark.parametrize("W", [32, 64])
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_overflow_rerun(gpu, W, mode):
+    """Row sums against the first block's maximum overflow: the exact rerun
+    (max-only pass, then the full pass with the true maximum) must reproduce
+    the oracle.  W = 32 is the key-split path (128 rows), W = 64 the other."""
+    spec = synth.AttnSpec(3, 32, W // 32, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 51, prefix_lens=[700, 3000, 96])
+    case = _plant_hot_keys(case, 52)
+    say(f"  W={W} mode={mode} P={case.prefix_lens.tolist()}")
+    for split in (0, 256):
+        out = run_case(gpu, case, mode, kv_split_tokens=split)
+        assert_attn_close(out, oracle_case(case, mode), f"rerun W={W} {mode} split={split}")
+
+
 @pytest.mark.parametrize("B", [8, 16])
 def test_small_blocks_block_causal(gpu, B):
     spec = synth.AttnSpec(2, B, 4, ("fixed", 0), 4, 4, 128)
