@@ -8,10 +8,16 @@
 // Decoding").  Ties go to the lowest index; the test is conf >= threshold.
 //
 // One HBM pass per row.  Each workgroup (256 threads) reduces one chunk of a
-// row; each thread streams 16-byte bf16 vectors, 2 in flight, and keeps
+// row; each thread streams 16-byte bf16 vectors (the next iteration's two
+// loads in flight while the current one is reduced) and keeps
 //   m       its running maximum,
-//   s       sum of exp(x - m), rescaled when m grows,
+//   s       sum of 2^(x log2(e) - mc), mc = m log2(e) rounded to fp32,
+//           rescaled when m grows,
 //   it_max  the iteration where m was first reached.
+// The exponent is one FMA per element.  Every exponent is off by the same
+// delta = m log2(e) - mc (the rounding residual of mc), so the confidence of
+// the maximum is 2^delta / s, and the entropy, which does not depend on the
+// reference, needs no correction.
 // Elements of one thread are visited in increasing index order, so its first
 // occurrence of m lies in iteration it_max.  Threads merge (max, rescaled
 // sum) in a fixed tree; then only the threads whose own maximum equals the
@@ -22,6 +28,8 @@
 // finalize kernel merges in chunk order, so results are bitwise reproducible.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "internal.h"
 
@@ -40,25 +48,38 @@ __device__ __forceinline__ float bf16_at(const uint16_t *p) {
   return __uint_as_float(static_cast<uint32_t>(*p) << 16);
 }
 
-// Exponent arguments below this are exactly 0 after exp2 in fp32; clamping
-// there keeps 0 * (-inf) out of the entropy sum.
+// Exponent arguments below this are exactly 0 after exp2 in fp32.  The
+// entropy sum adds 2^y * y; a -inf logit would add 0 * (-inf).  The main pass
+// does not clamp; a NaN sum sends the chunk through a second pass that clamps
+// y here (only rows holding -inf logits take it).
 constexpr float kYMin = -256.f;
 
+// The reference of a running maximum m: m log2(e) rounded to fp32.  All sums
+// are kept relative to it.  The product is formed by its own instruction:
+// fused into a following subtraction (d = ref(m) - ref(M)) it would lose the
+// rounding that the sums were accumulated against.
+__device__ __forceinline__ float ref_of(float m) {
+  float r;
+  asm("v_mul_f32 %0, %1, %2" : "=v"(r) : "v"(m), "v"(kLog2e));
+  return r;
+}
+
 // Merge partial (m, s, t) with (m2, s2, t2): the sums are rescaled to the
-// common max M.  With d = (m - M) log2(e): s -> 2^d s, t -> 2^d (t + d s).
+// common max M.  With d = ref(m) - ref(M): s -> 2^d s, t -> 2^d (t + d s).
 template <bool ENT>
 __device__ __forceinline__ void merge_ms(float &m, float &s, float &t, float m2, float s2, float t2) {
   const float M = fmaxf(m, m2);
   if (M == -INFINITY) return;     // both empty so far
   float a = 0.f, b = 0.f, ta = 0.f, tb = 0.f;
+  const float rM = ref_of(M);
   if (m != -INFINITY) {
-    const float d = (m - M) * kLog2e;
+    const float d = ref_of(m) - rM;
     const float f = __builtin_amdgcn_exp2f(d);
     a = s * f;
     if (ENT) ta = f * __builtin_fmaf(d, s, t);
   }
   if (m2 != -INFINITY) {
-    const float d = (m2 - M) * kLog2e;
+    const float d = ref_of(m2) - rM;
     const float f = __builtin_amdgcn_exp2f(d);
     b = s2 * f;
     if (ENT) tb = f * __builtin_fmaf(d, s2, t2);
@@ -83,19 +104,51 @@ __device__ __forceinline__ float entropy_nats(float s, float t) {
   return 0.69314718055994531f * (log2f(s) - t / s);
 }
 
+// max(a, b, c) in one instruction.  fmaxf would first quiet every input
+// (one more instruction each): the compiler cannot tell that floats made
+// from bf16 bits by shifts are not signalling NaNs.  NaN logits are outside
+// the contract; -inf is handled like any value.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Maximum of the 16 logits of one iteration: 8 three-input maxima.
+__device__ __forceinline__ float max16(const float (&x)[kU][8]) {
+  static_assert(kU == 2, "16 logits per iteration");
+  const float a = max3(x[0][0], x[0][1], x[0][2]);
+  const float b = max3(x[0][3], x[0][4], x[0][5]);
+  const float c = max3(x[0][6], x[0][7], x[1][0]);
+  const float d = max3(x[1][1], x[1][2], x[1][3]);
+  const float e = max3(x[1][4], x[1][5], x[1][6]);
+  const float f = max3(a, b, c);
+  const float g = max3(d, e, x[1][7]);
+  return max3(f, g, g);
+}
+
+// Eight bf16 logits of one 16-byte vector as floats.
+__device__ __forceinline__ void unpack8(const u32x4 &w, float x[8]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    x[2 * k] = bf16_lo(w[k]);
+    x[2 * k + 1] = bf16_hi(w[k]);
+  }
+}
+
+// Streaming load of one 16-byte vector: each logit is read once, so it is
+// not kept in cache.
+__device__ __forceinline__ u32x4 load16(const uint16_t *row, int64_t unit) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + unit * 8));
+}
+
 // Loads vector unit `unit` (elements 8*unit .. 8*unit+7) as 8 floats; elements
 // at or beyond `end` read as -inf.
 template <bool VEC>
 __device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int64_t end, float x[8]) {
   const int64_t e0 = unit * 8;
   if (VEC && e0 + 8 <= end) {
-    // Streaming load: each logit is read once, so it is not kept in cache.
-    const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + e0));
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      x[2 * k] = bf16_lo(w[k]);
-      x[2 * k + 1] = bf16_hi(w[k]);
-    }
+    unpack8(load16(row, unit), x);
   } else {
 #pragma unroll
     for (int k = 0; k < 8; ++k) x[k] = (e0 + k < end) ? bf16_at(row + e0 + k) : -INFINITY;
@@ -106,7 +159,10 @@ __device__ __forceinline__ void load_unit(const uint16_t *row, int64_t unit, int
 // for the threshold update, the row's prediction, confidence and entropy.
 template <bool ENT>
 __device__ __forceinline__ void decide(const EsParams &p, int64_t row, float m, float s, float t, int32_t idx) {
-  const float conf = 1.0f / s;          // correctly rounded division
+  // the maximum's own term is 2^delta, delta = m log2(e) - ref(m) exactly
+  // (0 when the product is exact, e.g. on a constant row of small integers)
+  const float delta = __builtin_fmaf(m, kLog2e, -ref_of(m));
+  const float conf = (delta == 0.f ? 1.0f : __builtin_amdgcn_exp2f(delta)) / s;   // correctly rounded division
   if (p.update) {
     p.pred[row] = idx;
     p.conf[row] = (m == -INFINITY) ? __builtin_nanf("") : conf;
@@ -141,29 +197,15 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   float m = -INFINITY, s = 0.f, t = 0.f;
   int32_t it_max = -1;
   int32_t it = 0;
-  for (int64_t base = u0; base < u1; base += kT * kU, ++it) {
-    float x[kU][8];
-#pragma unroll
-    for (int j = 0; j < kU; ++j) {
-      const int64_t unit = base + j * kT + tid;
-      if (unit < u1) {
-        load_unit<VEC>(rowp, unit, c1, x[j]);
-      } else {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) x[j][k] = -INFINITY;
-      }
-    }
-    float cm = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < kU; ++j)
-#pragma unroll
-      for (int k = 0; k < 8; k += 2) cm = fmaxf(cm, fmaxf(x[j][k], x[j][k + 1]));
+  // One iteration's 16 logits of this thread into the running (m, s, t).
+  auto accumulate = [&](const float (&x)[kU][8], auto clamp) {
+    const float cm = max16(x);
     if (cm > m) {
       if (m == -INFINITY) {
         s = 0.f;
         t = 0.f;
       } else {
-        const float d = (m - cm) * kLog2e;
+        const float d = ref_of(m) - ref_of(cm);
         const float f = __builtin_amdgcn_exp2f(d);
         if (ENT) t = f * __builtin_fmaf(d, s, t);
         s *= f;
@@ -171,43 +213,102 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
       m = cm;
       it_max = it;
     }
-    const float ms = (m == -INFINITY) ? 0.f : m;
+    const float nref = (m == -INFINITY) ? 0.f : -ref_of(m);
     float acc = 0.f, acct = 0.f;
 #pragma unroll
     for (int j = 0; j < kU; ++j)
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float y = (x[j][k] - ms) * kLog2e;
+        float y = __builtin_fmaf(x[j][k], kLog2e, nref);
+        if constexpr (decltype(clamp)::value) y = fmaxf(y, kYMin);
         const float e = __builtin_amdgcn_exp2f(y);
         acc += e;
-        if (ENT) acct = __builtin_fmaf(e, fmaxf(y, kYMin), acct);
+        if (ENT) acct = __builtin_fmaf(e, y, acct);
       }
     s += acc;
     if (ENT) t += acct;
-  }
+  };
+  // The whole chunk: iterations whose units all lie inside the chunk with
+  // unguarded vector loads, the next iteration's loads issued before the
+  // current one is reduced; then at most one guarded iteration.
+  auto pass = [&](auto clamp) {
+    m = -INFINITY;
+    s = 0.f;
+    t = 0.f;
+    it_max = -1;
+    it = 0;
+    constexpr int64_t per_iter = kT * kU;
+    int64_t base = u0;
+    if constexpr (VEC) {
+      const int64_t u_full = c1 / 8;      // units [u0, u_full) hold 8 logits of the chunk each
+      const int64_t n_full = u_full > u0 ? (u_full - u0) / per_iter : 0;
+      if (n_full > 0) {
+        u32x4 w[kU];
+#pragma unroll
+        for (int j = 0; j < kU; ++j) w[j] = load16(rowp, base + j * kT + tid);
+        for (int64_t i = 0; i < n_full; ++i, base += per_iter, ++it) {
+          float x[kU][8];
+#pragma unroll
+          for (int j = 0; j < kU; ++j) unpack8(w[j], x[j]);
+          if (i + 1 < n_full) {
+#pragma unroll
+            for (int j = 0; j < kU; ++j) w[j] = load16(rowp, base + per_iter + j * kT + tid);
+          }
+          accumulate(x, clamp);
+        }
+      }
+    }
+    for (; base < u1; base += per_iter, ++it) {
+      float x[kU][8];
+#pragma unroll
+      for (int j = 0; j < kU; ++j) {
+        const int64_t unit = base + j * kT + tid;
+        if (unit < u1) {
+          load_unit<VEC>(rowp, unit, c1, x[j]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) x[j][k] = -INFINITY;
+        }
+      }
+      accumulate(x, clamp);
+    }
+  };
+  pass(std::false_type{});
 
   // (max, rescaled sum) over the workgroup: wave butterfly, then the four
-  // wave results in wave order.
-  const float m_own = m;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float m2 = __shfl_xor(m, o);
-    const float s2 = __shfl_xor(s, o);
-    const float t2 = ENT ? __shfl_xor(t, o) : 0.f;
-    merge_ms<ENT>(m, s, t, m2, s2, t2);
-  }
+  // wave results in wave order.  Afterwards every thread holds the same
+  // (m, s, t).
   const int wave = tid / 64;
-  if ((tid & 63) == 0) {
-    sh_m[wave] = m;
-    sh_s[wave] = s;
-    sh_t[wave] = t;
-  }
-  __syncthreads();
-  m = sh_m[0];
-  s = sh_s[0];
-  t = sh_t[0];
+  float m_own = m;
+  auto reduce = [&]() {
+    m_own = m;
 #pragma unroll
-  for (int w = 1; w < kT / 64; ++w) merge_ms<ENT>(m, s, t, sh_m[w], sh_s[w], sh_t[w]);
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float m2 = __shfl_xor(m, o);
+      const float s2 = __shfl_xor(s, o);
+      const float t2 = ENT ? __shfl_xor(t, o) : 0.f;
+      merge_ms<ENT>(m, s, t, m2, s2, t2);
+    }
+    if ((tid & 63) == 0) {
+      sh_m[wave] = m;
+      sh_s[wave] = s;
+      sh_t[wave] = t;
+    }
+    __syncthreads();
+    m = sh_m[0];
+    s = sh_s[0];
+    t = sh_t[0];
+#pragma unroll
+    for (int w = 1; w < kT / 64; ++w) merge_ms<ENT>(m, s, t, sh_m[w], sh_s[w], sh_t[w]);
+  };
+  reduce();
+  if constexpr (ENT) {
+    if (t != t) {          // the chunk holds a -inf logit: clamped second pass
+      __syncthreads();     // every thread has read the shared partials
+      pass(std::true_type{});
+      reduce();
+    }
+  }
 
   // First index of the chunk maximum.  Only threads whose own maximum equals
   // it look: their first occurrence lies in iteration it_max, re-read once
