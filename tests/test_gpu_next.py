@@ -98,6 +98,33 @@ def test_update_full_parity(gpu, name, block, oe):
     say(f"  rows {L.shape[0]} actions {np.bincount(got['action'], minlength=4)} conf rel {rel:.1e}")
 
 
+def test_update_entropy_with_neg_inf_logits(gpu):
+    """64 x 131072 rows (vector loads, rows split over several workgroups) in
+    which a third of the vocabulary of the first 16 rows, and all but five
+    entries of row 3, are -inf: the entropy pass that meets a -inf logit goes
+    through its clamped second pass and must still match the oracle, and the
+    untouched rows must not change."""
+    L, cur, mid = update_case("single_p2048_k2_gqa16x4_d128", 6)
+    rng = np.random.default_rng(8)
+    V = L.shape[1]
+    Lm = L.clone()
+    for r in range(16):
+        Lm[r, torch.from_numpy(rng.choice(V - 1, V // 3, replace=False))] = float("-inf")
+    keep = rng.choice(V - 1, 5, replace=False)
+    row3 = torch.full((V,), float("-inf"), dtype=L.dtype)
+    row3[torch.from_numpy(keep)] = Lm[3, torch.from_numpy(keep)]
+    row3[torch.from_numpy(keep[:1])] = 4.0      # a clear maximum among the five
+    Lm[3] = row3
+    ref = oracle.threshold_update(Lm, cur, mid, 32, 0.5, 0.0, with_entropy=True)
+    safe(ref["conf"], cur, mid, 32, 0.5, 0.0)
+    got = run_update(gpu, Lm, cur, mid, 32, 0.5, 0.0)
+    compare_update(got, ref, "-inf logits")
+    assert np.all(np.isfinite(got["entropy"]))
+    plain = run_update(gpu, L, cur, mid, 32, 0.5, 0.0)
+    for key in ("conf", "entropy", "new_tokens"):
+        assert np.array_equal(got[key][16:], plain[key][16:]), key
+
+
 def test_update_long_context_sampled(gpu):
     """8192 x 131072 at the benchmark size: 24 blocks against the oracle, the
     counts and flags of all 256 blocks by their definitions."""
