@@ -53,7 +53,7 @@ struct AttnPlan {
 
 // Work units the chip runs at once: 256 CUs, one 256-row workgroup each.
 constexpr int64_t kConcurrentUnits = 256;
-constexpr int64_t kMinChunk = 256;      // shortest split, in keys
+constexpr int64_t kMinChunk = 128;      // shortest split, in keys
 
 mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_t block_size,
                           int32_t window_bound, int32_t fixed_window, AttnPlan *pl) {

@@ -650,16 +650,20 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   if (cu + r / p.num_q_heads >= p.total_q) return;
   const int64_t rowidx = static_cast<int64_t>(cu) * p.num_q_heads + r;
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
+  // every split below nsplit wrote this row (zeros and a -inf reference when
+  // it saw none of its keys), so the loads need no branch and unroll into
+  // independent groups
   float mmax = kNegInf;
+#pragma unroll 8
   for (int sp = 0; sp < nsplit; ++sp) mmax = fmaxf(mmax, p.part_ml[(sp * split_stride + rowidx) * 2]);
   float lsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
   for (int sp = 0; sp < nsplit; ++sp) {
     const float2 ml = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
-    if (ml.x == kNegInf) continue;          // split saw no key of this row
-    const float wgt = __builtin_amdgcn_exp2f(ml.x - mmax);
-    lsum += wgt * ml.y;
     const float4 po = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
+    const float wgt = ml.x == kNegInf ? 0.f : __builtin_amdgcn_exp2f(ml.x - mmax);   // no key of this row
+    lsum += wgt * ml.y;
     o.x += wgt * po.x;
     o.y += wgt * po.y;
     o.z += wgt * po.z;

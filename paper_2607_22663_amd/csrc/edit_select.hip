@@ -345,17 +345,31 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   decide<ENT>(p, row, m, s, t, idx);
 }
 
-// Rows reduced in several chunks: one thread per row merges the chunk
-// partials in chunk order (the kernel boundary makes them visible).
+// Rows reduced in several chunks: one wave per row merges the chunk partials
+// (the kernel boundary makes them visible).  Lane l merges chunks l, l + 64,
+// ... in order, then a butterfly combines the lanes; every step is a fixed,
+// commutative merge, so the result is the same on every lane and in every run.
 template <bool ENT>
 __global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (row >= p.rows) return;
+  const int lane = threadIdx.x & 63;
   const EsPartial *pp = p.partials + row * p.chunks;
-  float m = pp[0].m, s = pp[0].s, t = pp[0].t;
-  int32_t idx = pp[0].idx;
-  for (int c = 1; c < p.chunks; ++c) merge<ENT>(m, s, t, idx, pp[c].m, pp[c].s, pp[c].t, pp[c].idx);
-  decide<ENT>(p, row, m, s, t, idx);
+  float m = -INFINITY, s = 0.f, t = 0.f;
+  int32_t idx = INT32_MAX;
+  for (int c = lane; c < p.chunks; c += 64) {
+    const EsPartial q = pp[c];
+    merge<ENT>(m, s, t, idx, q.m, q.s, q.t, q.idx);
+  }
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float m2 = __shfl_xor(m, o);
+    const float s2 = __shfl_xor(s, o);
+    const float t2 = ENT ? __shfl_xor(t, o) : 0.f;
+    const int32_t i2 = __shfl_xor(idx, o);
+    merge<ENT>(m, s, t, idx, m2, s2, t2, i2);
+  }
+  if (lane == 0) decide<ENT>(p, row, m, s, t, idx);
 }
 
 // Threshold update, second step: one workgroup per block of block_size rows
@@ -417,9 +431,11 @@ __global__ __launch_bounds__(256) void threshold_block_kernel(EsParams p) {
 }  // namespace
 
 void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len) {
-  // Enough workgroups to cover 256 CUs several times over; a chunk keeps at
-  // least 4096 elements, one full iteration of the workgroup.
-  const int64_t target_wgs = 2048;
+  // Enough workgroups to cover the 256 CUs twice; a chunk keeps at least 4096
+  // elements, one full iteration of the workgroup.  (Measured on 64 rows of
+  // 131072: 512 workgroups of 4 iterations beat 2048 of one, whose time is
+  // dispatch and one memory round trip.)
+  const int64_t target_wgs = 512;
   int64_t c = 1;
   if (rows < target_wgs) {
     c = (target_wgs + rows - 1) / rows;
@@ -445,8 +461,8 @@ hipError_t launch_rows(const EsParams &p, bool vector_loads, hipStream_t stream)
     hipLaunchKernelGGL((edit_select_kernel<false, ENT>), grid, dim3(kT), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.chunks == 1) return e;
-  hipLaunchKernelGGL(edit_select_finalize_kernel<ENT>, dim3(static_cast<unsigned>((p.rows + 255) / 256)), dim3(256),
-                     0, stream, p);
+  hipLaunchKernelGGL(edit_select_finalize_kernel<ENT>, dim3(static_cast<unsigned>((p.rows + 3) / 4)), dim3(256), 0,
+                     stream, p);
   return hipGetLastError();
 }
 
