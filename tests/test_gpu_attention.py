@@ -257,3 +257,39 @@ def test_long_context_sampled(gpu):
     P = case.prefix_lens.numpy()
     seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 31})
     _sampled_parity(gpu, case, seqs, "long_context")
+
+
+def test_debug_check_rejects_bad_device_values(gpu, monkeypatch):
+    """MBE_DEBUG_CHECK=1: the attention call copies the lengths and the page
+    table to the host and returns MBE_ERR_BAD_VALUE, launching nothing, for a
+    page id outside the pool, a prefix beyond its bound or a window length
+    that is not a multiple of the block; a valid call still matches the oracle."""
+    spec = synth.AttnSpec(2, 32, 2, ("fixed", 0), 8, 2, 128)
+    case = synth.make_attention_case(spec, 71, prefix_lens=[100, 300])
+    c = case.to(DEV)
+    monkeypatch.setenv("MBE_DEBUG_CHECK", "1")
+    out = run_case(gpu, case)
+    assert_attn_close(out, oracle_case(case), "debug check on, valid input")
+
+    def call(**over):
+        a = dict(page_table=c.page_table, prefix_lens=c.prefix_lens, window_lens=c.window_lens)
+        kw = dict(max_prefix_len=300, max_window_len=64)
+        for key in list(over):
+            (a if key in a else kw)[key] = over[key]
+        with pytest.raises(gpu.MbeError) as ei:
+            gpu.window_attention(c.q, c.k_pages, c.v_pages, a["page_table"], a["prefix_lens"], a["window_lens"],
+                                 32, **kw)
+        torch.cuda.synchronize()
+        return ei.value
+
+    bad_pages = c.page_table.clone()
+    bad_pages[1, 3] = case.k_pages.shape[0] + 5
+    e = call(page_table=bad_pages)
+    assert e.status == 6 and "page_table[1][3]" in str(e), str(e)
+    neg_pages = c.page_table.clone()
+    neg_pages[0, 0] = -1
+    assert call(page_table=neg_pages).status == 6
+    e = call(max_prefix_len=200)
+    assert e.status == 6 and "prefix_lens[1]" in str(e), str(e)
+    e = call(window_lens=torch.tensor([64, 48], dtype=torch.int32, device=DEV))
+    assert e.status == 6 and "window_lens[1]" in str(e), str(e)
