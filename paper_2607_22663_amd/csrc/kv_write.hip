@@ -30,9 +30,12 @@ __global__ __launch_bounds__(256) void kv_write_kernel(KvWriteParams p) {
   const int p0 = max(start, page_slot * kPageSize);                          // positions [p0, p1) on this page
   const int p1 = min(start + len, (page_slot + 1) * kPageSize);
   if (p0 >= p1) return;
-  // first row of sequence b
+  // first row of sequence b: the lengths before it, summed across the lanes
+  // of the wave (independent loads, then a butterfly)
   int64_t row0 = 0;
-  for (int j = 0; j < b; ++j) row0 += min(max(p.lens[j], 0), p.max_len);
+  for (int j = threadIdx.x & 63; j < b; j += 64) row0 += min(max(p.lens[j], 0), p.max_len);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) row0 += __shfl_xor(row0, o);
   const int slot_row = min(page_slot, p.max_pages - 1);
   const int64_t page = min(max(p.page_table[static_cast<int64_t>(b) * p.max_pages + slot_row], 0), p.num_pages - 1);
   const int64_t page_base = (page * p.num_kv_heads + g) * static_cast<int64_t>(kPageSize) * D;   // elements
