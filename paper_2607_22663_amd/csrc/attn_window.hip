@@ -638,13 +638,17 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   constexpr int D4 = D / 4;
   const int64_t items = static_cast<int64_t>(W) * p.num_q_heads * D4;
   const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (item >= items) return;
+  // first query row of sequence b: the window lengths before it, summed
+  // across the lanes of the wave (before any lane leaves)
   int cu = 0;
   if (p.fixed_window >= 0) {
     cu = b * p.fixed_window;
   } else {
-    for (int j = 0; j < b; ++j) cu += min(max(p.window_lens[j], 0), p.max_window);
+    for (int j = threadIdx.x & 63; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
   }
+  if (item >= items) return;
   const int64_t r = item / D4;              // (window row, query head) within the sequence
   const int d0 = static_cast<int>(item % D4) * 4;
   if (cu + r / p.num_q_heads >= p.total_q) return;
