@@ -63,3 +63,22 @@ def test_random_shape_parity(gpu, seed):
     ref = oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
                                   case.window_lens, case.block_size, m)
     assert_attn_close(out.cpu(), ref, f"seed {seed}")
+
+
+def test_batch_beyond_dispatch_order_table(gpu):
+    """1100 short sequences: more than the 1024 whose longest-first dispatch
+    order fits in the kernel arguments, so the host lengths are ignored for
+    ordering and sequences run in natural order; results must not change."""
+    rng = np.random.default_rng(77)
+    n = 1100
+    spec = synth.AttnSpec(n, 16, 2, ("fixed", 0), 2, 1, 64)
+    P = [int(x) for x in rng.integers(0, 90, size=n)]
+    W = [int(x) * 16 for x in rng.integers(0, 3, size=n)]
+    case = synth.make_attention_case(spec, 78, prefix_lens=P, window_lens=W)
+    c = case.to(DEV)
+    out = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, 16,
+                               host_prefix_lens=case.prefix_lens, host_window_lens=case.window_lens)
+    torch.cuda.synchronize()
+    ref = oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
+                                  case.window_lens, 16)
+    assert_attn_close(out.cpu(), ref, "1100 sequences")
