@@ -134,10 +134,12 @@ _workspaces = {}
 
 
 def _workspace(kind: str, device: torch.device, nbytes: int) -> Optional[torch.Tensor]:
-    """Per-(kind, device) workspace, grown on demand (contents do not matter)."""
+    """Per-(kind, device, current stream) workspace, grown on demand (contents
+    do not matter).  Calls on one stream run in order, so they may share it;
+    calls on different streams get different buffers and never race."""
     if nbytes == 0:
         return None
-    key = (kind, device.index)
+    key = (kind, device.index, torch.cuda.current_stream(device).cuda_stream)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.empty(nbytes, dtype=torch.uint8, device=device)

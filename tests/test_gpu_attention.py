@@ -293,3 +293,24 @@ def test_debug_check_rejects_bad_device_values(gpu, monkeypatch):
     assert e.status == 6 and "prefix_lens[1]" in str(e), str(e)
     e = call(window_lens=torch.tensor([64, 48], dtype=torch.int32, device=DEV))
     assert e.status == 6 and "window_lens[1]" in str(e), str(e)
+
+
+def test_two_streams_get_their_own_workspace(gpu):
+    """Split-KV calls (which use the workspace) issued on two streams at once:
+    each matches the oracle, so the binding's per-stream buffers do not race."""
+    spec = synth.AttnSpec(1, 32, 2, ("fixed", 0), 16, 4, 128)
+    a = synth.make_attention_case(spec, 91, prefix_lens=[3000])
+    b = synth.make_attention_case(spec, 92, prefix_lens=[2500])
+    ca, cb = a.to(DEV), b.to(DEV)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            oa = gpu.window_attention(ca.q, ca.k_pages, ca.v_pages, ca.page_table, ca.prefix_lens, ca.window_lens,
+                                      32, kv_split_tokens=256)
+        with torch.cuda.stream(s2):
+            ob = gpu.window_attention(cb.q, cb.k_pages, cb.v_pages, cb.page_table, cb.prefix_lens, cb.window_lens,
+                                      32, kv_split_tokens=256)
+    torch.cuda.synchronize()
+    assert_attn_close(oa.cpu(), oracle_case(a), "stream 1")
+    assert_attn_close(ob.cpu(), oracle_case(b), "stream 2")
