@@ -114,17 +114,29 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return r;
 }
 
-// Maximum of the 16 logits of one iteration: 8 three-input maxima.
-__device__ __forceinline__ float max16(const float (&x)[kU][8]) {
-  static_assert(kU == 2, "16 logits per iteration");
-  const float a = max3(x[0][0], x[0][1], x[0][2]);
-  const float b = max3(x[0][3], x[0][4], x[0][5]);
-  const float c = max3(x[0][6], x[0][7], x[1][0]);
-  const float d = max3(x[1][1], x[1][2], x[1][3]);
-  const float e = max3(x[1][4], x[1][5], x[1][6]);
-  const float f = max3(a, b, c);
-  const float g = max3(d, e, x[1][7]);
-  return max3(f, g, g);
+// Maximum of the 8 kU logits of one iteration, three at a time (a tree of
+// about 4 kU three-input maxima).
+__device__ __forceinline__ float max_iter(const float (&x)[kU][8]) {
+  constexpr int N = 8 * kU;
+  float v[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) v[i] = x[i / 8][i % 8];
+  int n = N;
+#pragma unroll
+  for (int level = 0; level < 8; ++level) {
+    if (n == 1) break;
+    int m = 0;
+#pragma unroll
+    for (int i = 0; i < N; i += 3) {
+      if (i >= n) break;
+      if (i + 2 < n) v[m] = max3(v[i], v[i + 1], v[i + 2]);
+      else if (i + 1 < n) v[m] = max3(v[i], v[i + 1], v[i + 1]);
+      else v[m] = v[i];
+      ++m;
+    }
+    n = m;
+  }
+  return v[0];
 }
 
 // Eight bf16 logits of one 16-byte vector as floats.
@@ -199,7 +211,7 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   int32_t it = 0;
   // One iteration's 16 logits of this thread into the running (m, s, t).
   auto accumulate = [&](const float (&x)[kU][8], auto clamp) {
-    const float cm = max16(x);
+    const float cm = max_iter(x);
     if (cm > m) {
       if (m == -INFINITY) {
         s = 0.f;
