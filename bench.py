@@ -239,18 +239,18 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
     for r in sorted(stats, key=lambda r: -float(r.get("TotalDurationNs", 0))):
         lines.append(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f}% |")
-    if trace and line:
+    nxt = (line or {}).get("next_rows") or {}
+    if line and nxt:
+        lines += ["", "This run also times the calls outside the step (`next_rows` of the JSON line, at several "
+                      "shapes, including the graph-pool passes); the table above aggregates all their dispatches, "
+                      "and their HIP-event times per call are in the JSON line below."]
+    if trace and line and not nxt:
         steps = int(line["steps"])
         lines += ["", f"Average over the {steps} timed dispatches (the last {steps} of each kernel in the trace) "
                   "next to the same run's HIP-event timing:", "",
                   "| kernel | rocprofv3 trace average (us) | bench.py event average (us) |", "|---|---|---|"]
         ev = {"window_attention": line["attention"]["ms"] * 1e3,
               "edit_select": (line.get("edit_select") or {}).get("ms", 0) * 1e3}
-        nxt = line.get("next_rows") or {}
-        for key, name in (("kv_write", "kv_write"), ("tail_entropy_scores", "tail_entropy_scores"),
-                          ("select_start_block", "select_start_block")):
-            if key in nxt:
-                ev[name] = nxt[key]["ms"] * 1e3
         by = {}
         for r in sorted(trace, key=lambda r: int(r["Start_Timestamp"])):
             k = _kernel_key(r["Kernel_Name"])
@@ -260,9 +260,12 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
             d = d[-steps:]
             lines.append(f"| {k} | {sum(d) / len(d):.2f} | {ev[k]:.2f} |" if k in ev else
                          f"| {k} | {sum(d) / len(d):.2f} | (part of a call timed as a whole) |")
-        if nxt:
-            lines += ["", f"threshold_update (row pass with entropy + block pass) timed as one call: "
-                          f"{nxt['threshold_update']['ms'] * 1e3:.2f} us by HIP events."]
+        if "window_attention_merge" in by and "window_attention" in by:
+            a, m = by["window_attention"][-steps:], by["window_attention_merge"][-steps:]
+            lines += ["", f"The attention call is the main kernel plus the split merge: "
+                          f"{sum(a) / len(a) + sum(m) / len(m):.2f} us of kernel time per call by the trace, "
+                          f"{ev['window_attention']:.2f} us by HIP events. The events span the whole call; under "
+                          "rocprofv3 every dispatch carries extra launch overhead, which shows in short calls."]
     if line:
         lines += ["", "JSON line printed by the profiled run:", "", "```", json.dumps(line), "```"]
     with open(out_path, "w") as f:
