@@ -32,7 +32,7 @@ PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 DEFAULT_WORKLOAD = "long_context_b64_p4096to32768_k4"
 METRIC = "edit-window attention TFLOP/s (bf16) + edit-select GB/s, % of MI355X peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", f"hbm_traffic_{DEFAULT_WORKLOAD}.txt")
 CALIB_COPY_BYTES = 256 << 20     # the plain device copy bench.py runs once, for counter calibration
 
 
@@ -64,7 +64,7 @@ def kernel_source_hash():
 
 
 def read_traffic_file():
-    """profiles/hbm_traffic.txt: one `key=value ...` line per kernel."""
+    """The traffic summary: one `key=value ...` line per kernel."""
     out = {}
     try:
         with open(TRAFFIC_FILE) as f:
@@ -79,7 +79,8 @@ def read_traffic_file():
 
 
 def measured_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary
+    (profiles/hbm_traffic_<workload>.txt), if it
     was taken on the current kernel sources and this workload; else None."""
     e = read_traffic_file().get(kernel)
     if not e or e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
@@ -121,7 +122,8 @@ def _kernel_key(name):
 
 
 def summarize_pmc(dirs, workload):
-    """Writes profiles/hbm_traffic.txt from rocprofv3 --pmc runs of this script:
+    """Writes the HBM traffic summary (profiles/hbm_traffic_<workload>.txt) from
+    rocprofv3 --pmc runs of this script:
     FETCH_SIZE, then WRITE_SIZE, then optionally TCC_EA0_RDREQ_{32B,64B,128B}_sum
     plus TCC_EA0_RDREQ_sum.  FETCH_SIZE and WRITE_SIZE are each scaled by what
     the counter reads for the plain device copy of CALIB_COPY_BYTES that
@@ -131,10 +133,16 @@ def summarize_pmc(dirs, workload):
     sizes differs from the copy's."""
     fetch_dir, write_dir = dirs[0], dirs[1]
     req_dir = dirs[2] if len(dirs) > 2 else None
+    cmd = "python3 -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-next --no-others"
     lines = ["# HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE (KiB per dispatch),",
              "# each scaled by the same counter's reading for a plain 256 MiB device copy;",
              "# req_read_bytes = 32*RDREQ_32B + 64*RDREQ_64B + 128*RDREQ_128B (TCC to memory read requests).",
-             f"# workload {workload}; kernel_sha = hash of the kernel sources the counters were taken on"]
+             f"# workload {workload}; kernel_sha = hash of the kernel sources the counters were taken on",
+             "# commands (one MI355X, repository root), then python3 bench.py --summarize-pmc <the three folders>:",
+             f"#   rocprofv3 --pmc FETCH_SIZE -d {fetch_dir} -o run --output-format csv -- {cmd}",
+             f"#   rocprofv3 --pmc WRITE_SIZE -d {write_dir} -o run --output-format csv -- {cmd}",
+             f"#   rocprofv3 --pmc TCC_EA0_RDREQ_32B_sum TCC_EA0_RDREQ_64B_sum TCC_EA0_RDREQ_128B_sum TCC_EA0_RDREQ_sum "
+             f"-d {req_dir} -o run --output-format csv -- {cmd}"]
     scale = {}
     per_kernel = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
@@ -369,6 +377,73 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
     }
 
 
+def bench_other_workloads(mbe, headline, steps):
+    """The other configurations, each timed like the headline step (inputs in
+    HBM, 512 MiB read before every timed call, HIP events on the launch
+    stream): attention, and edit selection where the configuration has one.
+    Figures are per call; the attention share is against its own roofline."""
+    import torch
+    import synth
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flush.fill_(1)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        d = []
+        for _ in range(steps):
+            flush.view(torch.float32).sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            d.append(e0.elapsed_time(e1) / 1e3)
+        return float(np.mean(d)), float(np.median(d))
+
+    res = {}
+    for name, wl in synth.WORKLOADS.items():
+        ks = synth.SPAN_SWEEP_K if name.startswith("span_sweep") else (None,)
+        for k in ks:
+            if name == headline and k is None:
+                continue
+            tag = name if k is None else f"{name}_k{k}"
+            case = synth.workload_attention(name, k_blocks=k)
+            c = case.to(dev)
+            out = torch.empty_like(c.q)
+            mp, mw = int(case.prefix_lens.max()), int(case.window_lens.max())
+            t, tm = timed(lambda: mbe.window_attention(
+                c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, case.block_size, out=out,
+                max_prefix_len=mp, max_window_len=mw, host_prefix_lens=case.prefix_lens,
+                host_window_lens=case.window_lens))
+            flops, nbytes = attention_work(case)
+            roof = min(PEAK_BF16_TFLOPS, flops / nbytes * PEAK_HBM_GBS / 1e3)
+            tf = flops / t / 1e12
+            r = {"attention": {"ms": round(t * 1e3, 4), "ms_median": round(tm * 1e3, 4), "tflops": round(tf, 2),
+                               "pct_mfma_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+                               "roofline_tflops": round(roof, 1), "pct_of_roofline": round(100 * tf / roof, 2),
+                               "gbs": round(nbytes / t / 1e9, 1)}}
+            del c, out
+            if wl.edit is not None and k is None:
+                ec = synth.workload_edit(name)
+                L, cur = ec.logits.to(dev), ec.cur_tokens.to(dev)
+                R, V = L.shape
+                eo = (torch.empty(R, dtype=torch.int32, device=dev), torch.empty(R, dtype=torch.float32, device=dev),
+                      torch.empty(R, dtype=torch.uint8, device=dev))
+                t, tm = timed(lambda: mbe.edit_select(L, cur, ec.threshold, out=eo))
+                gbs = edit_bytes(R, V) / t / 1e9
+                r["edit_select"] = {"ms": round(t * 1e3, 4), "ms_median": round(tm * 1e3, 4), "rows": R, "vocab": V,
+                                    "gbs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / PEAK_HBM_GBS, 2)}
+                del L, cur, eo
+            res[tag] = r
+            print(f"[bench] {tag}: attention {r['attention']['ms']:.4f} ms", file=sys.stderr, flush=True)
+    del flush
+    return res
+
+
 def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_sample, edit_sample):
     """Times the fp64 oracle (as it stands) on a bounded sample of the same
     workload on the host cores, scaled to the whole step."""
@@ -433,10 +508,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
     ap.add_argument("--no-flush", action="store_true", help="do not flush the infinity cache before each step")
+    ap.add_argument("--no-others", action="store_true", help="skip timing the other configurations")
     ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
-                    help="write profiles/hbm_traffic.txt from rocprofv3 --pmc output folders (FETCH_SIZE, "
+                    help="write profiles/hbm_traffic_<workload>.txt from rocprofv3 --pmc output folders (FETCH_SIZE, "
                          "WRITE_SIZE, optionally the TCC_EA0_RDREQ_* request-size pass) and exit")
     ap.add_argument("--summarize-stats", nargs=4, metavar=("STATS_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
                     help="write a markdown summary of a rocprofv3 --kernel-trace --stats run and exit")
@@ -601,6 +677,8 @@ def main():
     }
     if edit_case is not None and not args.no_next:
         res["next_rows"] = bench_next_rows(mbe, attn_case, c, logits, cur, R, V, args.steps)
+    if not args.no_others:
+        res["other_workloads"] = bench_other_workloads(mbe, args.workload, min(args.steps, 20))
     if not args.no_cpu_baseline and edit_case is not None:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl, attn_case, edit_case, flops, e_bytes,
