@@ -52,6 +52,19 @@ def test_forced_split_kv(gpu, split):
     assert_attn_close(out, oracle_case(case), f"split {split}")
 
 
+@pytest.mark.parametrize("split", [0, 1 << 20])
+def test_prefix_of_140k_keys(gpu, split):
+    """A 140000-key prefix (8751 pages in its table row) beside a short one,
+    with the library's split choice and with one split over the whole prefix."""
+    spec = synth.AttnSpec(2, 16, 1, ("fixed", 0), 4, 2, 64)
+    case = synth.make_attention_case(spec, 41, prefix_lens=[140000, 5000], window_lens=[16, 16])
+    say(f"  kv_split_tokens {split} P={case.prefix_lens.tolist()}")
+    for mode in ("bidir", "block_causal"):
+        out = run_case(gpu, case, mode, kv_split_tokens=split, host_prefix_lens=case.prefix_lens,
+                       host_window_lens=case.window_lens)
+        assert_attn_close(out, oracle_case(case, mode), f"split {split} {mode}")
+
+
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
 def test_ragged_batch_with_poisoned_tails(gpu, D, mode):
