@@ -209,17 +209,20 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   __shared__ __align__(1024) char lds2[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds3[Tile<D>::kBufBytes];
 
-  // ---- work unit.  Groups (sequence rank, KV head, split) are dealt to the
-  // XCDs round-robin in dispatch order (workgroup id % 8 is the XCD), and the
-  // qtiles query tiles of a group, which read the same keys, take consecutive
-  // slots of the same XCD so that the second finds the keys in that XCD's L2.
+  // ---- work unit.  Groups (split, sequence rank, KV head), split slowest,
+  // are dealt to the XCDs round-robin in dispatch order (workgroup id % 8 is
+  // the XCD), and the qtiles query tiles of a group, which read the same keys,
+  // take consecutive slots of the same XCD so that the second finds the keys
+  // in that XCD's L2.  With the split slowest every XCD gets the same mix of
+  // first and later splits (later splits of short sequences have no work).
   const int64_t id = blockIdx.x;
   const int64_t slot = id / kXcds;
   const int64_t grp = (slot / p.qtiles) * kXcds + id % kXcds;
   if (grp >= p.groups) return;
   const int qtile = static_cast<int>(slot % p.qtiles);
-  const int split = static_cast<int>(grp % p.splits);
-  const int64_t rg = grp / p.splits;
+  const int64_t per_split = static_cast<int64_t>(p.batch) * p.num_kv_heads;
+  const int split = static_cast<int>(grp / per_split);
+  const int64_t rg = grp % per_split;
   const int rank = static_cast<int>(rg / p.num_kv_heads);
   const int g = static_cast<int>(rg % p.num_kv_heads);
   const int b = rank < p.seq_order_n ? p.seq_order[rank] : rank;

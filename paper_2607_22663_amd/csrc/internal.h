@@ -34,7 +34,7 @@ struct AttnParams {
   int32_t max_prefix, max_window;   // host-validated bounds; device lengths are clamped to them
   int32_t qtiles, splits, kv_chunk;
   int32_t key_split;          // 1, or 2 when a sequence has at most 128 rows per KV head
-  int64_t groups;             // (sequence rank, KV head, split) groups of qtiles work units
+  int64_t groups;             // (split, sequence rank, KV head) groups of qtiles work units
   int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
   // Sequences in the order their work is dispatched (longest first), when the
