@@ -657,24 +657,55 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   if (cu + r / p.num_q_heads >= p.total_q) return;
   const int64_t rowidx = static_cast<int64_t>(cu) * p.num_q_heads + r;
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
-  // every split below nsplit wrote this row (zeros and a -inf reference when
-  // it saw none of its keys), so the loads need no branch and unroll into
-  // independent groups
-  float mmax = kNegInf;
-#pragma unroll 8
-  for (int sp = 0; sp < nsplit; ++sp) mmax = fmaxf(mmax, p.part_ml[(sp * split_stride + rowidx) * 2]);
-  float lsum = 0.f;
+  // Every split below nsplit wrote this row (zeros and a -inf reference when
+  // it saw none of its keys).  Splits are read in chunks of C = 16, 8, 4, 2
+  // or 1 (the smallest that holds what is left, at most 16), all loads of a
+  // chunk issued together (past nsplit the last split is read again and
+  // weighted 0); the running maximum M and the sums are rescaled when a chunk
+  // raises M.  With at most 16 splits this is exactly the two-step form
+  // (M first, then the sums in split order).
+  float mrun = kNegInf, lsum = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-  for (int sp = 0; sp < nsplit; ++sp) {
-    const float2 ml = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
-    const float4 po = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
-    const float wgt = ml.x == kNegInf ? 0.f : __builtin_amdgcn_exp2f(ml.x - mmax);   // no key of this row
-    lsum += wgt * ml.y;
-    o.x += wgt * po.x;
-    o.y += wgt * po.y;
-    o.z += wgt * po.z;
-    o.w += wgt * po.w;
+  auto chunk = [&](int s0, auto csize) {
+    constexpr int C = decltype(csize)::value;
+    const int n = min(C, nsplit - s0);
+    float2 ml[C];
+    float4 po[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      const int64_t sp = s0 + min(j, n - 1);
+      ml[j] = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
+      po[j] = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
+    }
+    float cmax = mrun;
+#pragma unroll
+    for (int j = 0; j < C; ++j)
+      if (j < n) cmax = fmaxf(cmax, ml[j].x);
+    // old sums to the new maximum (nothing to rescale while M is -inf)
+    const float rescale = mrun == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mrun - cmax);
+    lsum *= rescale;
+    o.x *= rescale;
+    o.y *= rescale;
+    o.z *= rescale;
+    o.w *= rescale;
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      const float wgt = (j < n && ml[j].x != kNegInf) ? __builtin_amdgcn_exp2f(ml[j].x - cmax) : 0.f;
+      lsum += wgt * ml[j].y;
+      o.x += wgt * po[j].x;
+      o.y += wgt * po[j].y;
+      o.z += wgt * po[j].z;
+      o.w += wgt * po[j].w;
+    }
+    mrun = cmax;
+  };
+  for (int s0 = 0; s0 < nsplit;) {
+    const int left = nsplit - s0;
+    if (left > 8) { chunk(s0, std::integral_constant<int, 16>{}); s0 += 16; }
+    else if (left > 4) { chunk(s0, std::integral_constant<int, 8>{}); s0 += 8; }
+    else if (left > 2) { chunk(s0, std::integral_constant<int, 4>{}); s0 += 4; }
+    else if (left == 2) { chunk(s0, std::integral_constant<int, 2>{}); s0 += 2; }
+    else { chunk(s0, std::integral_constant<int, 1>{}); s0 += 1; }
   }
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   uint2 st;
