@@ -228,19 +228,6 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int b = rank < p.seq_order_n ? p.seq_order[rank] : rank;
 
   const int G = p.group;
-  // lengths are clamped to the host-validated bounds, so a wrong device value
-  // can give wrong numbers but never an access outside q, out or the workspace
-  const int P = min(max(p.prefix_lens[b], 0), p.max_prefix);
-  const int W = p.fixed_window >= 0 ? p.fixed_window : min(max(p.window_lens[b], 0), p.max_window);
-  const int n_all = P + W;
-  const int M = G * W;
-  const int row0 = qtile * kRowsPerTile;
-  if (row0 >= M) return;
-  const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
-  if (split >= nsplit) return;
-  const int kb = split * p.kv_chunk;
-  const int ke = min(n_all, kb + p.kv_chunk);
-
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -248,10 +235,31 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int h = lane >> 5;       // which half of the 32x32 MFMA layout
   const int wrow = KS == 2 ? (wave & 1) : wave;   // 64-row slice of this wave
   const int kown = KS == 2 ? (wave >> 1) : 0;     // 32-key block of each tile (KS = 2)
+  const int wv = __builtin_amdgcn_readfirstlane(wave);   // wave index as a scalar
+  const int kb = split * p.kv_chunk;
+
+  // The reads below depend only on b and are issued together: the lengths
+  // and the page of the first tile that this wave loads.  With a fixed
+  // window, window_lens may be absent and prefix_lens is read in its place
+  // and ignored.
+  const bool fixed = p.fixed_window >= 0;
+  const int32_t P_dev = p.prefix_lens[b];
+  const int32_t W_dev = (fixed ? p.prefix_lens : p.window_lens)[b];
+  const int pid0 = wave_page(p, b, kb, wv);
+  // lengths are clamped to the host-validated bounds, so a wrong device value
+  // can give wrong numbers but never an access outside q, out or the workspace
+  const int W = fixed ? p.fixed_window : min(max(W_dev, 0), p.max_window);
+  const int P = min(max(P_dev, 0), p.max_prefix);
+  const int M = G * W;
+  const int row0 = qtile * kRowsPerTile;
+  const int n_all = P + W;
+  const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
+  // no rows in this query tile, or a split past the sequence's last
+  if (row0 >= M || split >= nsplit) return;
 
   // first query row of sequence b
   int cu = 0;
-  if (p.fixed_window >= 0) {
+  if (fixed) {
     cu = b * p.fixed_window;
   } else {
     for (int j = lane; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
@@ -259,8 +267,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
   }
 
-  // ---- this lane's two query rows (one per 32-row block of the wave)
-  int lim[2];
+  // ---- this lane's two query rows (one per 32-row block of the wave), and
+  // their Q^T operands in registers: lane (c, h) holds dims 16kk + 8h .. +7
   bool valid[2];
   int64_t qoff[2];
 #pragma unroll
@@ -270,20 +278,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     const int i = valid[qb] ? r / G : 0;
     const int hq = g * G + (valid[qb] ? r % G : 0);
     qoff[qb] = (static_cast<int64_t>(cu + i) * p.num_q_heads + hq) * D;
-    int n = n_all;
-    if (MODE == 1) n = min(n_all, P + (i / p.block_size + 1) * p.block_size);
-    lim[qb] = valid[qb] ? min(n, ke) : ke;
   }
-  // keys any row of this workgroup can see
-  int kend = ke;
-  if (MODE == 1) {
-    const int r_last = min(M, row0 + kRowsPerTile) - 1;
-    const int i_last = r_last / G;
-    kend = min(ke, P + (i_last / p.block_size + 1) * p.block_size);
-  }
-  const int ntiles = kend > kb ? (kend - kb + kKeyTile - 1) / kKeyTile : 0;
-
-  // ---- Q^T operands in registers: lane (c, h) holds dims 16kk + 8h .. +7
   constexpr int KK = D / 16;
   bf16x8 qreg[2][KK];
 #pragma unroll
@@ -295,6 +290,27 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       else
         qreg[qb][kk] = bf16x8{};
     }
+
+  // ---- key range of this split
+  const int ke = min(n_all, kb + p.kv_chunk);
+  int lim[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    int n = n_all;
+    if (MODE == 1) {
+      const int i = (row0 + wrow * kRowsPerWave + qb * 32 + c) / G;   // window position of the row
+      n = min(n_all, P + (i / p.block_size + 1) * p.block_size);
+    }
+    lim[qb] = valid[qb] ? min(n, ke) : ke;
+  }
+  // keys any row of this workgroup can see
+  int kend = ke;
+  if (MODE == 1) {
+    const int r_last = min(M, row0 + kRowsPerTile) - 1;
+    const int i_last = r_last / G;
+    kend = min(ke, P + (i_last / p.block_size + 1) * p.block_size);
+  }
+  const int ntiles = kend > kb ? (kend - kb + kKeyTile - 1) / kKeyTile : 0;
 
   // ---- loop-invariant LDS operand offsets of this lane
   // K: row perm_row(c) (+32 for the second key block), chunk 2kk + h
@@ -402,7 +418,6 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // ---- key loop: tile t lives in buffer t % 4; tiles t+1..t+3 are in flight
   // while tile t is computed.  pid holds the page ids of the next tile to load.
-  const int wv = __builtin_amdgcn_readfirstlane(wave);   // wave index as a scalar
   uint32_t kload_off[Tile<D>::kLoads];
   k_load_offsets<D>(kload_off);
   int pid = 0;                                             // this wave's page of the next tile
@@ -437,7 +452,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   };
   auto prologue = [&]() {
-    pid = wave_page(p, b, kb, wv);
+    pid = pid0;
     for (int t = 0; t < 3 && t < ntiles; ++t) issue(t, buf_of(t));
     land(min(2, ntiles - 1));
     fix_tail(0);
