@@ -52,6 +52,21 @@ def test_forced_split_kv(gpu, split):
     assert_attn_close(out, oracle_case(case), f"split {split}")
 
 
+@pytest.mark.parametrize("nsplit", [2, 3, 5, 8, 9, 16, 17, 32, 33, 40])
+def test_merge_chunk_boundaries(gpu, nsplit):
+    """Split counts on both sides of the merge's chunk sizes (16, 8, 4, 2, 1):
+    a 64-key split over P + W = 64 * nsplit - 8 keys, with a ragged second
+    sequence of fewer splits and one whose window is empty."""
+    spec = synth.AttnSpec(3, 16, 2, ("fixed", 0), 8, 2, 64)
+    P0 = 64 * nsplit - 8 - 32
+    case = synth.make_attention_case(spec, 90 + nsplit, prefix_lens=[P0, max(0, P0 // 3), 100],
+                                     window_lens=[32, 16, 0], tail_fill=float("nan"))
+    say(f"  nsplit {nsplit} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
+    for mode in ("bidir", "block_causal"):
+        out = run_case(gpu, case, mode, kv_split_tokens=64)
+        assert_attn_close(out, oracle_case(case, mode), f"nsplit {nsplit} {mode}")
+
+
 @pytest.mark.parametrize("split", [0, 1 << 20])
 def test_prefix_of_140k_keys(gpu, split):
     """A 140000-key prefix (8751 pages in its table row) beside a short one,
