@@ -141,6 +141,14 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
 size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv,
                                            const mbe_attn_opts *opts, int32_t block_size);
 
+/* Workspace bytes block_diffusion_attention needs for these shapes and
+ * options.  Its split plan takes W_b = block_size for every sequence (and
+ * the host prefix lengths when given), so it can differ from
+ * mbe_window_attention_workspace_size with the same opts.
+ * Returns (size_t)-1 if the arguments are invalid. */
+size_t mbe_block_diffusion_workspace_size(const mbe_paged_kv *paged_kv,
+                                          const mbe_attn_opts *opts, int32_t block_size);
+
 /* Confidence-based edit selection (paper, Sec. "Configurable threshold
  * decoding", Eq. (1), the token-to-token set), for every row r:
  *   a       = lowest index v with logits[r][v] maximal

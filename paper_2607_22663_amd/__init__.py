@@ -26,7 +26,7 @@ STATUS_NAMES = {0: "MBE_OK", 1: "MBE_ERR_NULL_ARG", 2: "MBE_ERR_BAD_SHAPE", 3: "
 MASK_MODES = {"bidir": 0, "block_causal": 1}
 
 EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
-           "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_threshold_update",
+           "mbe_block_diffusion_workspace_size", "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_threshold_update",
            "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores", "mbe_select_start_block",
            "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error")
 ACTIONS = {"keep": 0, "unmask": 1, "force_unmask": 2, "edit": 3}
@@ -82,6 +82,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_window_attention_workspace_size.argtypes = [ctypes.POINTER(PagedKV),
                                                             ctypes.POINTER(AttnOpts), i32]
         lib.mbe_window_attention_workspace_size.restype = sz
+        lib.mbe_block_diffusion_workspace_size.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts), i32]
+        lib.mbe_block_diffusion_workspace_size.restype = sz
         lib.mbe_edit_select.argtypes = [vp, i64, i64, i64, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]
         lib.mbe_edit_select.restype = ctypes.c_int
         lib.mbe_edit_select_workspace_size.argtypes = [i64, i64]
@@ -276,9 +278,10 @@ def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, bloc
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), None,
                     None, 0, stream)
-    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+    need = lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
     if need == ctypes.c_size_t(-1).value:
-        need = 0
+        _check("block_diffusion_attention", lib.block_diffusion_attention(
+            None, ctypes.byref(kv), None, None, int(block_size), None, ctypes.byref(opts)))
     ws = _workspace("attn", q.device, need)
     opts.workspace = _ptr(ws)
     opts.workspace_bytes = need

@@ -302,6 +302,15 @@ size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const m
   return pl.bytes;
 }
 
+size_t mbe_block_diffusion_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts,
+                                          int32_t block_size) {
+  AttnPlan pl;
+  if (!opts || block_size < 1) return static_cast<size_t>(-1);
+  if (plan_attention(paged_kv, opts, block_size, block_size, block_size, &pl) != MBE_OK)
+    return static_cast<size_t>(-1);
+  return pl.bytes;
+}
+
 size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab) {
   if (rows < 0 || vocab < 0) return static_cast<size_t>(-1);
   if (rows == 0 || vocab == 0) return 0;

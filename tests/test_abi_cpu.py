@@ -5,6 +5,7 @@ import math
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2607_22663_amd as mbe
@@ -27,7 +28,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert len(names) == 13, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(mbe.EXPORTS)
@@ -85,6 +86,27 @@ def test_attention_null_pointers_and_workspace(lib):
     opts.workspace, opts.workspace_bytes = ctypes.c_void_p(256), need - 1
     st, msg = _attn(lib, kv, opts)
     assert st == 4
+
+
+def test_block_diffusion_workspace_size_is_what_the_call_requires(lib):
+    """block_diffusion_attention plans with W_b = block_size and the host
+    prefix lengths; its size query must give exactly the bytes the call then
+    requires (the window-attention query, without host window lengths here,
+    plans from the bounds and asks for less)."""
+    kv = _kv(pages=20000)
+    P = np.array([100, 16000, 200, 300, 50, 8000, 10, 64], dtype=np.int32)
+    opts = _opts(batch=8, total_q=8 * 32, max_prefix_len=16000, max_window_len=32, max_pages_per_seq=1100,
+                 host_prefix_lens=P.ctypes.data_as(ctypes.c_void_p))
+    need = lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32)
+    assert 0 < need != ctypes.c_size_t(-1).value
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32) < need
+    opts.workspace, opts.workspace_bytes = ctypes.c_void_p(256 * 1024), need - 1
+    st = lib.block_diffusion_attention(ctypes.c_void_p(64), ctypes.byref(kv), ctypes.c_void_p(8),
+                                       ctypes.c_void_p(8), 32, ctypes.c_void_p(128), ctypes.byref(opts))
+    assert st == 4 and f"required {need}" in lib.mbe_last_error().decode()
+    assert lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 0) == \
+        ctypes.c_size_t(-1).value
+    assert lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), None, 32) == ctypes.c_size_t(-1).value
 
 
 def test_attention_empty_batch_is_ok_without_launch(lib):

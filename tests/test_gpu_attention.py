@@ -197,6 +197,20 @@ def test_block_diffusion_baseline(gpu):
     assert torch.equal(w_bi, out.cpu()) and torch.equal(w_bc, out.cpu())
 
 
+def test_block_diffusion_ragged_prefixes(gpu):
+    """Ragged prefixes with host lengths: the block-diffusion call plans its
+    splits from them, and its workspace comes from its own size query."""
+    spec = synth.AttnSpec(5, 32, 1, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 19, prefix_lens=[100, 16000, 0, 3000, 544])
+    c = case.to(DEV)
+    out = gpu.block_diffusion_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, 32,
+                                        host_prefix_lens=case.prefix_lens)
+    torch.cuda.synchronize()
+    ref = oracle.block_diffusion_attention(case.q, case.k_pages, case.v_pages, case.page_table,
+                                           case.prefix_lens, 32)
+    assert_attn_close(out.cpu(), ref, "block_diffusion_attention, ragged prefixes")
+
+
 def test_block_causal_equals_stacked_single_blocks_on_gpu(gpu):
     spec = synth.AttnSpec(1, 32, 3, ("fixed", 0), 16, 4, 128)
     case = synth.make_attention_case(spec, 12, prefix_lens=[512])
