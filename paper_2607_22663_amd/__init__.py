@@ -26,9 +26,9 @@ STATUS_NAMES = {0: "MBE_OK", 1: "MBE_ERR_NULL_ARG", 2: "MBE_ERR_BAD_SHAPE", 3: "
 MASK_MODES = {"bidir": 0, "block_causal": 1}
 
 EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
-           "mbe_block_diffusion_workspace_size", "mbe_edit_select", "mbe_edit_select_workspace_size", "mbe_threshold_update",
-           "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores", "mbe_select_start_block",
-           "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error")
+           "mbe_block_diffusion_workspace_size", "mbe_edit_select", "mbe_edit_select_workspace_size",
+           "mbe_threshold_update", "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores",
+           "mbe_select_start_block", "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error")
 ACTIONS = {"keep": 0, "unmask": 1, "force_unmask": 2, "edit": 3}
 REFRESH_MODES = {"changed": 0, "changed_and_later": 1}
 
