@@ -20,6 +20,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -56,10 +57,16 @@ def edit_bytes(rows, vocab):
 
 
 def kernel_source_hash():
+    """Hash of the code of the timed kernels' sources: comments, trailing
+    blanks and empty lines are dropped first, so that an edit of a comment
+    keeps counters taken on the same code valid."""
     h = hashlib.sha256()
     for f in ("attn_window.hip", "edit_select.hip", "internal.h"):
-        with open(os.path.join(ROOT, "paper_2607_22663_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2607_22663_amd", "csrc", f)) as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", "", src)
+        h.update("\n".join(ln.rstrip() for ln in src.splitlines() if ln.strip()).encode())
     return h.hexdigest()[:16]
 
 
@@ -137,7 +144,8 @@ def summarize_pmc(dirs, workload):
     lines = ["# HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE (KiB per dispatch),",
              "# each scaled by the same counter's reading for a plain 256 MiB device copy;",
              "# req_read_bytes = 32*RDREQ_32B + 64*RDREQ_64B + 128*RDREQ_128B (TCC to memory read requests).",
-             f"# workload {workload}; kernel_sha = hash of the kernel sources the counters were taken on",
+             f"# workload {workload}; kernel_sha = hash of the code (comments and blank lines dropped) of the "
+             "kernel sources the counters were taken on",
              "# commands (one MI355X, repository root), then python3 bench.py --summarize-pmc <the three folders>:",
              f"#   rocprofv3 --pmc FETCH_SIZE -d {fetch_dir} -o run --output-format csv -- {cmd}",
              f"#   rocprofv3 --pmc WRITE_SIZE -d {write_dir} -o run --output-format csv -- {cmd}",

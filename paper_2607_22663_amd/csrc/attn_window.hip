@@ -27,7 +27,8 @@
 //
 // Softmax: base 2, fp32, against a fixed reference per row instead of a
 // running maximum, so inside the key loop the O accumulators are touched by
-// MFMA only.  The reference is the row's maximum over its first key tile.
+// MFMA only.  The reference is the row's maximum over the first 32 keys of
+// its split.
 // Later exponentials 2^(s - ref) may exceed 1; bf16 P and fp32 sums share
 // fp32's exponent range, so nothing overflows unless a later score exceeds
 // the reference by about 2^127.  The row sum is checked once at the end of
@@ -46,9 +47,9 @@
 // fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled and a
 // V page ([D][16 keys]) with the two 8-key halves of every other group of 8
 // dims swapped, so that the MFMA operand reads are free of bank conflicts.
-// Workgroup ids are mapped so that each XCD runs a contiguous range of work
-// units and the query tiles sharing a key range run back to back on the same
-// XCD (shared L2).
+// Work groups (split, sequence, KV head) are dealt round-robin to the XCDs,
+// and the query tiles sharing a key range run back to back on the same XCD
+// (shared L2).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
