@@ -57,7 +57,6 @@ constexpr int64_t kMinChunk = 128;      // shortest split, in keys
 
 mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_t block_size,
                           int32_t window_bound, int32_t fixed_window, AttnPlan *pl) {
-  auto fixed_window_of = [fixed_window](const mbe_attn_opts *, int32_t) { return fixed_window; };
   if (!kv) return fail(MBE_ERR_NULL_ARG, "paged_kv is NULL");
   if (!o) return fail(MBE_ERR_NULL_ARG, "opts is NULL");
   if (kv->page_size != mbe::kPageSize)
@@ -94,14 +93,14 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   const int64_t base_units = static_cast<int64_t>(o->batch) * kv->num_kv_heads * pl->qtiles;
 
   // Host copies of the lengths, when given, refine the plan.
-  const bool host = o->host_prefix_lens && (fixed_window_of(o, window_bound) >= 0 || o->host_window_lens) &&
+  const bool host = o->host_prefix_lens && (fixed_window >= 0 || o->host_window_lens) &&
                     o->batch > 0 && o->batch <= mbe::kMaxOrderedSeqs;
   std::vector<int64_t> n_seq;   // keys each sequence's units read
   if (host) {
     n_seq.resize(o->batch);
     for (int b = 0; b < o->batch; ++b) {
       const int64_t P = o->host_prefix_lens[b];
-      const int64_t W = fixed_window_of(o, window_bound) >= 0 ? fixed_window_of(o, window_bound) : o->host_window_lens[b];
+      const int64_t W = fixed_window >= 0 ? fixed_window : o->host_window_lens[b];
       if (P < 0 || P > o->max_prefix_len || W < 0 || W > window_bound)
         return fail(MBE_ERR_BAD_SHAPE, "host lengths of sequence %d (%lld, %lld) exceed the bounds", b,
                     static_cast<long long>(P), static_cast<long long>(W));
@@ -117,7 +116,7 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
       if (host) {
         for (int b = 0; b < o->batch; ++b) {
           if (n_seq[b] == 0) continue;
-          const int64_t W = fixed_window_of(o, window_bound) >= 0 ? fixed_window_of(o, window_bound) : o->host_window_lens[b];
+          const int64_t W = fixed_window >= 0 ? fixed_window : o->host_window_lens[b];
           const int64_t qt = (pl->group * W + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile;
           u += kv->num_kv_heads * qt * ((n_seq[b] + c - 1) / c);
         }
