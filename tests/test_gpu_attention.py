@@ -356,3 +356,45 @@ def test_two_streams_get_their_own_workspace(gpu):
     torch.cuda.synchronize()
     assert_attn_close(oa.cpu(), oracle_case(a), "stream 1")
     assert_attn_close(ob.cpu(), oracle_case(b), "stream 2")
+
+
+def test_pool_beyond_2_31_elements(gpu):
+    """K/V pools of 300000 pages x 4 KV heads x 16 x 128 (2.46e9 elements,
+    4.9 GB each): page ids near the end lie past 2^31 elements, so the page
+    addressing of attention and of the KV write-back must be 64-bit.  One
+    sequence (prefix 4000, window 64) whose pages are spread over the whole
+    pool, its window on the pool's last page; the oracle runs on a compact
+    copy of the referenced pages."""
+    Hkv, D, Hq, B = 4, 128, 16, 32
+    npages, P, W = 300_000, 4000, 64
+    n_pg = (P + W + 15) // 16
+    rng = np.random.default_rng(123)
+    ids = rng.choice(npages - 1, size=n_pg, replace=False).astype(np.int64)
+    ids[(P + W - 1) // 16] = npages - 1                   # the window's last page is the pool's last
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(7)
+    K = torch.empty(npages, Hkv, 16, D, dtype=torch.bfloat16, device=DEV).normal_(generator=gen)
+    V = torch.empty(npages, Hkv, D, 16, dtype=torch.bfloat16, device=DEV).normal_(generator=gen)
+    q = torch.from_numpy(rng.normal(size=(W, Hq, D)).astype(np.float32)).to(torch.bfloat16)
+    pt = torch.from_numpy(ids.astype(np.int32)[None, :])
+    plen = torch.tensor([P], dtype=torch.int32)
+    wlen = torch.tensor([W], dtype=torch.int32)
+    say(f"  pool {npages} pages, last element offset {npages * Hkv * 16 * D:.3e}; page ids up to {ids.max()}")
+    out = gpu.window_attention(q.to(DEV), K, V, pt.to(DEV), plen.to(DEV), wlen.to(DEV), B)
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(ids).to(DEV)
+    Kc, Vc = K[idx].cpu(), V[idx].cpu()
+    compact = torch.arange(n_pg, dtype=torch.int32)[None, :]
+    ref = oracle.window_attention(q, Kc, Vc, compact, plen, wlen, B)
+    assert_attn_close(out.cpu(), ref, "attention over a pool beyond 2^31 elements")
+    # KV write-back of the window tokens: lands on pages including the last
+    kn = torch.from_numpy(rng.normal(size=(W, Hkv, D)).astype(np.float32)).to(torch.bfloat16)
+    vn = torch.from_numpy(rng.normal(size=(W, Hkv, D)).astype(np.float32)).to(torch.bfloat16)
+    gpu.kv_write(K, V, pt.to(DEV), plen.to(DEV), wlen.to(DEV), kn.to(DEV), vn.to(DEV))
+    torch.cuda.synchronize()
+    rk, rv = oracle.kv_write(Kc.view(torch.int16), Vc.view(torch.int16), compact.numpy(), plen.numpy(), wlen.numpy(),
+                             kn.view(torch.int16), vn.view(torch.int16))
+    assert np.array_equal(K[idx].cpu().view(torch.int16).numpy(), rk)
+    assert np.array_equal(V[idx].cpu().view(torch.int16).numpy(), rv)
+    del K, V
+    torch.cuda.empty_cache()

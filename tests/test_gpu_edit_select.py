@@ -145,3 +145,26 @@ def test_zero_rows(gpu):
     n, c, ch = gpu.edit_select(torch.empty(0, 128, dtype=torch.bfloat16, device=DEV),
                                torch.empty(0, dtype=torch.int32, device=DEV), 0.9)
     assert n.numel() == 0
+
+
+def test_logits_beyond_2_31_elements(gpu):
+    """17024 x 131072 logits (2.23e9 elements, 4.5 GB): the rows past 2^31
+    elements need 64-bit row offsets.  Seeded N(0, 3) drawn on the device, a
+    +8 peak in every other sampled row; 64 sampled rows, the last ones
+    included, against the oracle."""
+    R, V = 17024, 131072
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(11)
+    L = torch.empty(R, V, dtype=torch.bfloat16, device=DEV).normal_(0.0, 3.0, generator=gen)
+    rng = np.random.default_rng(12)
+    rows = np.unique(np.concatenate([[0, R // 2, R - 2, R - 1], rng.choice(R, 60, replace=False)]))
+    for r, col in zip(rows[::2], rng.integers(0, V, size=rows[::2].size)):
+        L[int(r), int(col)] = (L[int(r)].float().max() + 8.0).to(torch.bfloat16)
+    cur = torch.from_numpy(rng.integers(0, V, size=R).astype(np.int32))
+    say(f"  {R} x {V} = {R * V:.3e} elements")
+    res = run(gpu, L, cur, 0.9)
+    sel = torch.from_numpy(rows)
+    ref = oracle.edit_select(L[sel.to(DEV)].cpu(), cur[sel], 0.9)
+    check(res, ref, 0.9, "logits beyond 2^31 elements", rows=rows)
+    del L
+    torch.cuda.empty_cache()
