@@ -99,9 +99,11 @@ typedef struct {
                                  the longest sequences first; they must equal the
                                  device values.  Ignored when batch > 1024.          */
   void *workspace;            /* device memory of at least
-                                 mbe_window_attention_workspace_size bytes, 256-byte
-                                 aligned, any contents (split-KV partial results);
-                                 may be NULL when that size is 0                     */
+                                 mbe_window_attention_workspace_size bytes
+                                 (mbe_block_diffusion_workspace_size for
+                                 block_diffusion_attention), 256-byte aligned, any
+                                 contents (split-KV partial results); may be NULL
+                                 when that size is 0                                 */
   size_t workspace_bytes;
   void *stream;               /* hipStream_t                                        */
 } mbe_attn_opts;
