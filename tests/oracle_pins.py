@@ -153,6 +153,32 @@ def check_full_window_is_dense(impl):
                      f"dense block-causal h={h}")
 
 
+def check_prefix_and_window_is_sdpa(impl):
+    """P > 0 and k > 1 against torch's fp64 SDPA over the gathered P + W keys:
+    bidirectional = no mask at all (every window row sees the whole prefix and
+    window, Eq. (4)); block-causal = the prefix plus window blocks up to the
+    row's own, an explicit boolean mask built from block ids."""
+    case = small_case(29, batch=2, B=8, k=3, Hq=4, Hkv=2, D=16, prefix=(21, 40))
+    B = case.block_size
+    ob = impl.window_attention(case.q, case.k_pages, case.v_pages, case.page_table,
+                               case.prefix_lens, case.window_lens, B, impl.MASK_BIDIR)
+    oc = impl.window_attention(case.q, case.k_pages, case.v_pages, case.page_table,
+                               case.prefix_lens, case.window_lens, B, impl.MASK_BLOCK_CAUSAL)
+    cu = case.cu_q
+    G = case.num_q_heads // case.num_kv_heads
+    for b in range(case.batch):
+        P, W = int(case.prefix_lens[b]), int(case.window_lens[b])
+        key_blk = torch.cat([torch.full((P,), -1), torch.arange(W) // B])     # prefix keys: block -1
+        row_blk = torch.arange(W) // B
+        mask = key_blk[None, :] <= row_blk[:, None]
+        for h in range(case.num_q_heads):
+            K, V = loop_gather(case, b, h // G, P + W)
+            qm = q_rows(case, b)[:, h]
+            assert_close(ob[cu[b]:cu[b + 1], h], sdpa(qm, K, V).numpy(), 1e-12, f"bidir vs SDPA b={b} h={h}")
+            assert_close(oc[cu[b]:cu[b + 1], h], sdpa(qm, K, V, mask).numpy(), 1e-12,
+                         f"block-causal vs SDPA b={b} h={h}")
+
+
 def check_probs_normalised(impl):
     case = small_case(17, batch=2, B=4, k=3, prefix=(12, 3), q_scale=4.0)
     for mode in (impl.MASK_BIDIR, impl.MASK_BLOCK_CAUSAL):
@@ -273,7 +299,8 @@ def check_golden_attention(impl):
 
 
 ATTENTION_CHECKS = [check_k1_is_block_diffusion, check_block_causal_is_stacked_blocks,
-                    check_full_window_is_dense, check_probs_normalised, check_invariances,
+                    check_full_window_is_dense, check_prefix_and_window_is_sdpa, check_probs_normalised,
+                    check_invariances,
                     check_closed_forms, check_golden_attention]
 
 
