@@ -262,3 +262,47 @@ def test_refresh_validation(lib):
     assert lib.mbe_refresh_blocks(_vp(16), 2, 4, 2, _vp(16), None) == 3
     assert lib.mbe_refresh_blocks(None, 2, 4, 0, _vp(16), None) == 1
     assert lib.mbe_refresh_blocks(None, 0, 4, 0, None, None) == 0
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    """include/mbe.h compiles as C99 with every warning an error, and a C
+    program links against libmbe.so and calls the host-only entry points
+    (status strings, workspace sizes, a validation failure)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_mbe.c"
+    src.write_text(r'''
+#include <stdio.h>
+#include <string.h>
+#include "mbe.h"
+int main(void) {
+  mbe_paged_kv kv = {0};
+  mbe_attn_opts o;
+  size_t n;
+  memset(&o, 0, sizeof(o));
+  kv.page_size = 16; kv.num_kv_heads = 4; kv.head_dim = 128; kv.num_pages = 10;
+  o.batch = 1; o.num_q_heads = 16; o.max_pages_per_seq = 10; o.total_q = 64;
+  o.max_prefix_len = 64; o.max_window_len = 64;
+  n = mbe_window_attention_workspace_size(&kv, &o, 32);
+  if (n != 0) return 1;
+  kv.head_dim = 96;
+  if (mbe_window_attention(NULL, &kv, NULL, NULL, NULL, 32, NULL, &o) != MBE_ERR_UNSUPPORTED) return 2;
+  if (strstr(mbe_last_error(), "head_dim") == NULL) return 3;
+  if (strcmp(mbe_status_string(MBE_OK), "ok") != 0) return 4;
+  if (mbe_edit_select_workspace_size(64, 131072) == 0) return 5;
+  if (mbe_threshold_update_workspace_size(-1, 1) != (size_t)-1) return 6;
+  printf("ok\n");
+  return 0;
+}
+''')
+    exe = tmp_path / "use_mbe"
+    libdir = os.path.dirname(mbe.LIB_PATH)
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(ROOT, "include"),
+                        str(src), "-o", str(exe), "-L", libdir, "-lmbe", f"-Wl,-rpath,{libdir}"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
