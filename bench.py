@@ -228,6 +228,37 @@ def summarize_mfma(pmc_dir, bench_stdout, out_path, command, workload):
     print("\n".join(lines))
 
 
+def summarize_counters(pmc_dir, kernel, out_path, command, workload):
+    """Markdown table of one rocprofv3 --pmc pass: each counter's average per
+    dispatch of one kernel (a key of _KERNELS), with the LDS bank-conflict
+    share and the VALU issue share when their counters are there."""
+    rows = [r for r in _counter_rows(pmc_dir) if _kernel_key(r["Kernel_Name"]) == kernel]
+    per = {}
+    for r in rows:
+        per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    avg = {k: sum(v) / len(v) for k, v in per.items()}
+    n = len(rows) // max(1, len(per))
+    lines = [f"# {kernel}: rocprofv3 counters", "", f"Workload {workload}, one rocprofv3 --pmc pass, average per "
+             f"dispatch over {n} dispatches.", "", "Command:", "", "```", command, "```", "",
+             "| counter | value per dispatch |", "|---|---|"]
+    for k in sorted(avg):
+        lines.append(f"| {k} | {avg[k]:.4g} |")
+    lines.append("")
+    if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_LDS_IDX_ACTIVE"):
+        lines.append(f"- LDS bank-conflict cycles per LDS-active cycle: "
+                     f"{avg['SQ_LDS_BANK_CONFLICT'] / avg['SQ_LDS_IDX_ACTIVE']:.2e} "
+                     "(SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE).")
+    if "SQ_ACTIVE_INST_VALU" in avg and avg.get("SQ_WAVE_CYCLES"):
+        lines.append(f"- VALU issue share of wave cycles: {100 * avg['SQ_ACTIVE_INST_VALU'] / avg['SQ_WAVE_CYCLES']:.1f}% "
+                     "(SQ_ACTIVE_INST_VALU / SQ_WAVE_CYCLES).")
+    if "SQ_WAIT_INST_ANY" in avg and avg.get("SQ_WAVE_CYCLES"):
+        lines.append(f"- Waiting for any instruction's inputs: {100 * avg['SQ_WAIT_INST_ANY'] / avg['SQ_WAVE_CYCLES']:.1f}% "
+                     "of wave cycles (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES).")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_stats(stats_dir, bench_stdout, out_path, command):
     """Writes a short markdown summary of a rocprofv3 --kernel-trace --stats run
     of this script: rocprofv3's per-kernel statistics, the average over the
@@ -524,6 +555,9 @@ def main():
                          "WRITE_SIZE, optionally the TCC_EA0_RDREQ_* request-size pass) and exit")
     ap.add_argument("--summarize-stats", nargs=4, metavar=("STATS_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
                     help="write a markdown summary of a rocprofv3 --kernel-trace --stats run and exit")
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("PMC_DIR", "KERNEL", "OUT_MD"),
+                    help="write OUT_MD from a rocprofv3 --pmc pass over one kernel (the command is --counter-command)")
+    ap.add_argument("--counter-command", default="")
     ap.add_argument("--summarize-mfma", nargs=4, metavar=("PMC_DIR", "BENCH_STDOUT", "OUT_MD", "COMMAND"),
                     help="write a markdown summary of a rocprofv3 --pmc pass of MFMA counters and exit")
     args = ap.parse_args()
@@ -535,6 +569,10 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma, args.workload)
+        return
+    if args.summarize_counters:
+        pmc_dir, kernel, out_md = args.summarize_counters
+        summarize_counters(pmc_dir, kernel, out_md, args.counter_command, args.workload)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
