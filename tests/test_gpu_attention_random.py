@@ -2,11 +2,12 @@
 
 Each seed draws a batch of 1..5 sequences with ragged prefixes (0..1500
 tokens, any value), windows of 0..k blocks (block size 8, 16 or 32), 1, 2 or
-4 KV heads with 1, 2 or 4 query heads each, head_dim 64 or 128, a mask mode,
-a split-KV chunk (library's choice or forced), host lengths or bounds only,
-and extra unreferenced pages; every pool slot no sequence covers holds NaN.
-Together the draws reach every kernel variant: one or two waves per 64 rows
-(at most 128 rows per KV head), split and unsplit, masked tails.
+4 KV heads with 1, 2, 4 or 8 query heads each, head_dim 64 or 128, a mask
+mode, a split-KV chunk (library's choice or forced), host lengths or bounds
+only, and extra unreferenced pages; every pool slot no sequence covers holds
+NaN.  Together the draws reach every kernel variant: one or two waves per 64
+rows (at most 128 rows per KV head), one to four query tiles per KV head,
+split and unsplit, masked tails.
 """
 import numpy as np
 import pytest
@@ -26,13 +27,13 @@ def draw(seed):
     B = int(rng.choice([8, 16, 32]))
     k = int(rng.integers(1, 5))
     Hkv = int(rng.choice([1, 2, 4]))
-    G = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([1, 2, 4, 8]))
     D = int(rng.choice([64, 128]))
     P = [int(x) for x in rng.integers(0, 1501, size=batch)]
     W = [int(x) * B for x in rng.integers(0, k + 1, size=batch)]
     W[int(rng.integers(batch))] = k * B
     mode = str(rng.choice(["bidir", "block_causal"]))
-    split = int(rng.choice([0, 0, 64, 192, 512]))
+    split = int(rng.choice([0, 0, 64, 128, 192, 512]))
     host = bool(rng.integers(2))
     extra = int(rng.integers(0, 4))
     spec = synth.AttnSpec(batch, B, k, ("fixed", 0), Hkv * G, Hkv, D)
@@ -41,7 +42,7 @@ def draw(seed):
     return case, mode, split, host
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(48))
 def test_random_shape_parity(gpu, seed):
     case, mode, split, host = draw(seed)
     say(f"  seed {seed}: B={case.block_size} G={case.num_q_heads // case.num_kv_heads} Hkv={case.num_kv_heads} "
