@@ -304,6 +304,8 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
     if cur_tokens.shape[0] != rows:
         raise ValueError("cur_tokens must have one entry per row")
     v = logits.shape[1] if vocab is None else int(vocab)
+    if not 0 <= v <= logits.shape[1]:
+        raise ValueError(f"vocab {v} outside [0, {logits.shape[1]}] (the columns of logits)")
     ld = logits.stride(0) if rows > 1 else max(logits.shape[1], 1)
     if out is None:
         new = torch.empty(rows, dtype=torch.int32, device=dev)
@@ -336,6 +338,8 @@ def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_
     if cur_tokens.shape[0] != rows:
         raise ValueError("cur_tokens must have one entry per row")
     v = logits.shape[1] if vocab is None else int(vocab)
+    if not 0 <= v <= logits.shape[1]:
+        raise ValueError(f"vocab {v} outside [0, {logits.shape[1]}] (the columns of logits)")
     ld = logits.stride(0) if rows > 1 else max(logits.shape[1], 1)
     nblk = rows // block_size if block_size > 0 else 0
     if out is None:

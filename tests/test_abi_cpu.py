@@ -7,6 +7,7 @@ import re
 
 import numpy as np
 import pytest
+import torch
 
 import paper_2607_22663_amd as mbe
 
@@ -306,3 +307,14 @@ int main(void) {
     assert r.returncode == 0, r.stderr
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
+
+
+def test_binding_rejects_vocab_beyond_the_columns():
+    """The binding checks vocab against the logits' columns before any call
+    (the C ABI only sees the row stride)."""
+    logits = torch.zeros(2, 10, dtype=torch.bfloat16)
+    cur = torch.zeros(2, dtype=torch.int32)
+    with pytest.raises(ValueError, match="vocab"):
+        mbe.edit_select(logits, cur, 0.9, vocab=11)
+    with pytest.raises(ValueError, match="vocab"):
+        mbe.threshold_update(logits, cur, 9, 2, 0.5, 0.0, vocab=11)
