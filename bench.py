@@ -548,7 +548,7 @@ def main():
     ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
     ap.add_argument("--no-flush", action="store_true", help="do not flush the infinity cache before each step")
     ap.add_argument("--no-others", action="store_true", help="skip timing the other configurations")
-    ap.add_argument("--attn-sample", type=int, default=24, help="sequences the CPU oracle times")
+    ap.add_argument("--attn-sample", type=int, default=28, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
                     help="write profiles/hbm_traffic_<workload>.txt from rocprofv3 --pmc output folders (FETCH_SIZE, "
