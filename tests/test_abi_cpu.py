@@ -320,19 +320,23 @@ def test_binding_rejects_vocab_beyond_the_columns():
         mbe.threshold_update(logits, cur, 9, 2, 0.5, 0.0, vocab=11)
 
 
-def test_error_string_is_per_thread(lib):
+def test_error_string_is_per_thread():
     """Concurrent calls (ctypes drops the GIL) each read their own failure
     from mbe_last_error(): the error string is thread-local."""
     import threading
+    lib = mbe.load()      # the binding's current structure classes (another test reloads the module)
     errors = []
 
     def worker(hd):
-        kv = _kv(head_dim=hd)
-        for _ in range(200):
-            st, msg = _attn(lib, kv, _opts())
-            if st != 3 or f"head_dim {hd}" not in msg:
-                errors.append((hd, st, msg))
-                return
+        try:
+            kv = _kv(head_dim=hd)
+            for _ in range(200):
+                st, msg = _attn(lib, kv, _opts())
+                if st != 3 or f"head_dim {hd}" not in msg:
+                    errors.append((hd, st, msg))
+                    return
+        except Exception as e:      # an exception in a thread would not fail the test by itself
+            errors.append((hd, "exception", repr(e)))
 
     threads = [threading.Thread(target=worker, args=(hd,)) for hd in (32, 48, 80, 96, 100, 256, 512, 1000)]
     for t in threads:
