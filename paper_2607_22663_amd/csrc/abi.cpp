@@ -152,13 +152,19 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   if (pl->slots_per_xcd * mbe::kXcds > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "grid too large");
 
   // Longest sequences first (stable), so the short ones fill in at the end.
+  // (no table when that is the natural order, e.g. one sequence or equal
+  // lengths: the kernel then skips reading it)
   pl->order_n = 0;
   if (host) {
     std::vector<int32_t> idx(o->batch);
     for (int b = 0; b < o->batch; ++b) idx[b] = b;
     std::stable_sort(idx.begin(), idx.end(), [&](int32_t x, int32_t y) { return n_seq[x] > n_seq[y]; });
-    for (int b = 0; b < o->batch; ++b) pl->order[b] = static_cast<uint16_t>(idx[b]);
-    pl->order_n = o->batch;
+    bool natural = true;
+    for (int b = 0; b < o->batch; ++b) {
+      pl->order[b] = static_cast<uint16_t>(idx[b]);
+      natural = natural && idx[b] == b;
+    }
+    pl->order_n = natural ? 0 : o->batch;
   }
 
   pl->bytes = 0;
