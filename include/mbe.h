@@ -19,7 +19,9 @@
  *     are clamped into range, so a bad table gives wrong numbers but never an
  *     out-of-bounds access.  With the environment variable MBE_DEBUG_CHECK=1,
  *     the attention calls copy the lengths and the page table to the host
- *     (synchronously) and return MBE_ERR_BAD_VALUE on a violation.
+ *     (on the call's stream, then synchronising it) and return
+ *     MBE_ERR_BAD_VALUE on a violation; calls made while the stream is being
+ *     captured into a graph are not checked.
  *   - An error from the HIP runtime is returned as MBE_ERR_HIP, with the HIP
  *     error string in mbe_last_error().
  *   - No global mutable state except the thread-local error string.  Calls

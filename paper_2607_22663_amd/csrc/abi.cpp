@@ -181,12 +181,21 @@ mbe_status debug_check_attention(const mbe_paged_kv *kv, const int32_t *page_tab
                                  const int32_t *window_lens, int32_t block_size, int32_t fixed_window,
                                  const mbe_attn_opts *o) {
   const int B = o->batch;
+  const hipStream_t stream = static_cast<hipStream_t>(o->stream);
+  // A copy cannot be recorded into a graph: calls made while the stream is
+  // capturing are not checked.
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return hip_fail(e, "MBE_DEBUG_CHECK capture query");
+  if (cs != hipStreamCaptureStatusNone) return MBE_OK;
+  // copies on the call's stream, so they see what the caller wrote there before
   std::vector<int32_t> P(B), W(B, fixed_window), T(static_cast<size_t>(B) * o->max_pages_per_seq);
-  hipError_t e = hipMemcpy(P.data(), prefix_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost);
+  e = hipMemcpyAsync(P.data(), prefix_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
   if (e == hipSuccess && fixed_window < 0)
-    e = hipMemcpy(W.data(), window_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost);
+    e = hipMemcpyAsync(W.data(), window_lens, B * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
   if (e == hipSuccess && !T.empty())
-    e = hipMemcpy(T.data(), page_table, T.size() * sizeof(int32_t), hipMemcpyDeviceToHost);
+    e = hipMemcpyAsync(T.data(), page_table, T.size() * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) return hip_fail(e, "MBE_DEBUG_CHECK copy");
   int64_t tq = 0;
   for (int b = 0; b < B; ++b) {

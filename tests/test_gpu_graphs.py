@@ -82,3 +82,34 @@ def test_graph_pool_rejects_unknown_shapes(gpu):
         pool.capture(1, 48)
     with pytest.raises(KeyError):
         pool.replay(1, 32)
+
+
+def test_capture_with_debug_check_enabled(gpu, monkeypatch):
+    """MBE_DEBUG_CHECK=1 copies the lengths to the host, which a graph cannot
+    record: calls under capture skip the check, so capture and replay still
+    work, while eager calls on the same inputs are checked."""
+    from paper_2607_22663_amd.graphs import EditPassGraphs
+    monkeypatch.setenv("MBE_DEBUG_CHECK", "1")
+    spec = synth.AttnSpec(2, 32, 1, ("fixed", 0), 4, 4, 64)
+    case = synth.make_attention_case(spec, 29, prefix_lens=[64, 100])
+    c = case.to(DEV)
+    V, B = 256, 32
+    pool = EditPassGraphs(k_pages=c.k_pages, v_pages=c.v_pages, max_batch=2, max_window=32, block_size=B,
+                          num_q_heads=4, max_pages_per_seq=case.page_table.shape[1], max_prefix_len=100, vocab=V,
+                          mask_id=V - 1)
+    pool.capture(2, 32)
+    rng = np.random.default_rng(30)
+    inp = pool.inputs(2, 32)
+    inp["q"].copy_(c.q)
+    inp["page_table"].copy_(c.page_table)
+    inp["prefix_lens"].copy_(c.prefix_lens)
+    inp["logits"].copy_(torch.from_numpy(rng.normal(0, 3, (64, V)).astype(np.float32)).to(torch.bfloat16).to(DEV))
+    inp["cur_tokens"].copy_(torch.from_numpy(rng.integers(0, V - 1, 64).astype(np.int32)).to(DEV))
+    pool.replay(2, 32)
+    torch.cuda.synchronize()
+    got = pool.outputs(2, 32)["attention"].clone()
+    W = torch.full((2,), 32, dtype=torch.int32, device=DEV)
+    att = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, W, B,
+                               max_prefix_len=100, max_window_len=32)
+    torch.cuda.synchronize()
+    assert torch.equal(got, att)
