@@ -10,7 +10,8 @@
  *     keeps no pointer after a call returns and allocates nothing.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
  *     stream).  They never synchronise; results are valid once the stream has
- *     been synchronised.
+ *     been synchronised.  Kernels are launched on the current HIP device;
+ *     every buffer and the stream must belong to it.
  *   - Arguments are validated on the host before any HIP call.  A failed
  *     check returns a non-OK status, launches nothing and writes nothing.
  *     mbe_last_error() then holds a thread-local description.

@@ -12,6 +12,7 @@ cannot be loaded, every call raises; there is no other implementation.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 import threading
 from typing import Optional
@@ -108,6 +109,19 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_last_error.restype = ctypes.c_char_p
         _lib = lib
         return lib
+
+
+def _on_device(fn):
+    """Runs a call with the current HIP device set to the device of its first
+    (tensor) argument: the library launches on the current device."""
+    @functools.wraps(fn)
+    def wrapper(*args, **kwargs):
+        t = args[0] if args else None
+        if isinstance(t, torch.Tensor) and t.is_cuda and t.device.index != torch.cuda.current_device():
+            with torch.cuda.device(t.device):
+                return fn(*args, **kwargs)
+        return fn(*args, **kwargs)
+    return wrapper
 
 
 def _check(call, status):
@@ -216,6 +230,7 @@ def _host_i32(x, batch, name):
     return a
 
 
+@_on_device
 def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size, *,
                      out=None, mask_mode="bidir", softmax_scale=None, max_prefix_len=None,
                      max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None,
@@ -261,6 +276,7 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     return out
 
 
+@_on_device
 def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size, *,
                               out=None, softmax_scale=None, max_prefix_len=None, kv_split_tokens=0,
                               host_prefix_lens=None):
@@ -291,6 +307,7 @@ def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, bloc
     return out
 
 
+@_on_device
 def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
     """Edit selection (paper, Eq. (1), token-to-token set).  logits: bf16
     [rows, row_stride] (the first `vocab` columns are used; default all).
@@ -322,6 +339,7 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
     return new, conf, changed
 
 
+@_on_device
 def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_edit, *, vocab=None,
                      with_entropy=False, out=None, workspace=None):
     """Full threshold update (paper, Eq. (1) with force-unmask).  Rows form
@@ -361,6 +379,7 @@ def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_
     return out
 
 
+@_on_device
 def tail_entropy_scores(entropy, block_size, rho, *, out=None):
     """Eq. (5): mean of the ceil(rho * B) largest entropies of every block of
     block_size consecutive rows.  entropy: float32 [num_blocks * B]."""
@@ -374,6 +393,7 @@ def tail_entropy_scores(entropy, block_size, rho, *, out=None):
     return scores
 
 
+@_on_device
 def select_start_block(scores, current_block, k_max, *, out=None):
     """Eq. (6): start block of every sequence's window.  scores: float32
     [batch, max_blocks]; current_block: int32 [batch]."""
@@ -388,6 +408,7 @@ def select_start_block(scores, current_block, k_max, *, out=None):
     return start
 
 
+@_on_device
 def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max_len=None):
     """Write recomputed K/V (bf16 [total_tokens, heads, D]) into the paged
     pools in place: token t of sequence b goes to position start_pos[b] + t."""
@@ -409,6 +430,7 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max
         _ptr(v_new), _stream(dev)))
 
 
+@_on_device
 def refresh_blocks(block_changed, mode="changed", *, out=None):
     """Blocks to recompute after editing from per-block changed flags
     (uint8 [batch, num_blocks]); mode "changed" or "changed_and_later"."""
