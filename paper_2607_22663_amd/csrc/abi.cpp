@@ -11,6 +11,7 @@
 #include <cstdlib>
 #include <algorithm>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -47,13 +48,153 @@ struct AttnPlan {
   int32_t group = 0, qtiles = 0, splits = 1, kv_chunk = 0;
   int64_t groups = 0, slots_per_xcd = 0;
   size_t part_o_off = 0, part_ml_off = 0, bytes = 0;
-  int32_t order_n = 0;
-  uint16_t order[mbe::kMaxOrderedSeqs];
+  int32_t order_kind = mbe::kOrderNone, order_n = 0;
+  uint16_t order[mbe::kMaxOrder];
 };
 
 // Work units the chip runs at once: 256 CUs, one 256-row workgroup each.
 constexpr int64_t kConcurrentUnits = 256;
 constexpr int64_t kMinChunk = 128;      // shortest split, in keys
+constexpr int kCusPerXcd = 32;
+
+// Cost model of a dispatch table, in 64-key tile times: a work unit costs
+// its tiles plus a workgroup's start (Q and the first tiles' latency, about
+// four tile times); splitting adds the merge (its launch, and reading the
+// partial results at roughly 8 MB per tile time).
+constexpr double kUnitStartTiles = 4.0;
+constexpr double kMergeStartTiles = 1.5;
+constexpr double kMergeBytesPerTile = 8e6;
+constexpr double kMinPlanGain = 0.01;   // a shorter split must beat the default by this share
+
+struct SeqWork {
+  int64_t n;      // keys the sequence's units read (0: no rows)
+  int64_t w;      // window rows
+  int32_t nq;     // query tiles with rows
+};
+
+struct UnitSchedule {
+  double finish = -1.0;           // modelled completion in tile times; < 0: no table
+  int32_t order_n = 0;            // workgroups: 8 x the longest XCD list
+  uint16_t order[mbe::kMaxOrder]; // workgroup id -> work unit (kNoUnit: none)
+};
+
+// Dispatch table for splits of c keys.  The work units that have rows and
+// keys form groups (the query tiles of one (split, sequence, KV head), which
+// read the same keys); the groups are dealt largest first to the XCD with
+// the least work so far, and an XCD's units take its slots (workgroup ids x,
+// x + 8, ...) in that order, so that each XCD starts its longest units first
+// and the hardware, which starts an XCD's next workgroup on whichever of its
+// CUs frees first, balances them.  The modelled finish replays exactly
+// that.  No table (finish < 0) with more than kMaxOrder units, more than
+// kMaxOrder / 8 on one XCD, or a unit index beyond 16 bits.
+void schedule_units(const std::vector<SeqWork> &seqs, int32_t hkv, int32_t qtiles, int32_t hq, int32_t head_dim,
+                    int64_t max_kv, int64_t c, UnitSchedule *out) {
+  out->finish = -1.0;
+  const int64_t batch = static_cast<int64_t>(seqs.size());
+  const int64_t splits = std::max<int64_t>(1, (max_kv + c - 1) / c);
+  const int64_t per_split = batch * hkv;
+  if (per_split * splits * qtiles >= mbe::kNoUnit) return;
+  auto nsplit_of = [&](int64_t n) { return std::min<int64_t>(splits, std::max<int64_t>(1, (n + c - 1) / c)); };
+  int64_t total = 0;
+  bool same_nq = true;
+  for (const SeqWork &sq : seqs)
+    if (sq.n > 0) {
+      total += nsplit_of(sq.n) * hkv * sq.nq;
+      same_nq = same_nq && sq.nq == seqs[0].nq;
+    }
+  if (total == 0 || total > mbe::kMaxOrder) return;
+
+  struct Grp {
+    float cost;
+    int32_t grp;
+    int16_t nq, tiles;
+  };
+  Grp grps[mbe::kMaxOrder];
+  int ng = 0;
+  double merge_bytes = 0.0;
+  bool any_split = false;
+  auto add = [&](int64_t b, int64_t sp, int64_t keys) {
+    const int t = static_cast<int>(std::min<int64_t>((keys + mbe::kKeyTile - 1) / mbe::kKeyTile, 32767));
+    const int32_t nq = seqs[b].nq;
+    for (int32_t g = 0; g < hkv; ++g)
+      grps[ng++] = {static_cast<float>(nq * (t + kUnitStartTiles)), static_cast<int32_t>(sp * per_split + b * hkv + g),
+                    static_cast<int16_t>(nq), static_cast<int16_t>(t)};
+  };
+  // Largest first.  With the same query tiles for every sequence this order
+  // needs no sort over the groups: every full-length split (c keys) first,
+  // then each sequence's last split by its length.
+  struct Last {
+    int64_t keys, b;
+  };
+  Last last[mbe::kMaxOrder];
+  int nl = 0;
+  for (int64_t b = 0; b < batch; ++b) {
+    const SeqWork &sq = seqs[b];
+    if (sq.n == 0) continue;
+    const int64_t nsb = nsplit_of(sq.n);
+    if (nsb > 1) {
+      any_split = true;
+      // partial O and (reference, sum) read per split, bf16 O written
+      merge_bytes += static_cast<double>(sq.w) * hq * (nsb * (head_dim + 2) * 4.0 + head_dim * 2.0);
+    }
+    for (int64_t sp = 0; sp + 1 < nsb; ++sp) add(b, sp, c);
+    last[nl++] = {sq.n - (nsb - 1) * c, b};
+  }
+  std::sort(last, last + nl, [](const Last &x, const Last &y) { return x.keys != y.keys ? x.keys > y.keys : x.b < y.b; });
+  for (int i = 0; i < nl; ++i) add(last[i].b, nsplit_of(seqs[last[i].b].n) - 1, last[i].keys);
+  if (!same_nq) std::stable_sort(grps, grps + ng, [](const Grp &x, const Grp &y) { return x.cost > y.cost; });
+
+  constexpr int kSlots = mbe::kMaxOrder / mbe::kXcds;
+  uint16_t unit[mbe::kXcds][kSlots];
+  int16_t tiles[mbe::kXcds][kSlots];
+  int len[mbe::kXcds] = {};
+  double load[mbe::kXcds] = {};
+  for (int i = 0; i < ng; ++i) {
+    int x = 0;                     // least-loaded XCD, lowest index on ties (selects, no branches)
+    double lx = load[0];
+    for (int j = 1; j < mbe::kXcds; ++j) {
+      const bool lt = load[j] < lx;
+      x = lt ? j : x;
+      lx = lt ? load[j] : lx;
+    }
+    if (len[x] + grps[i].nq > kSlots) return;
+    load[x] += grps[i].cost;
+    for (int q = 0; q < grps[i].nq; ++q) {
+      unit[x][len[x]] = static_cast<uint16_t>(grps[i].grp * qtiles + q);
+      tiles[x][len[x]++] = grps[i].tiles;
+    }
+  }
+  // replay: per XCD, each unit starts on the CU that frees first: the first
+  // 32 take one CU each, the rest go through a min-heap of the CU free times
+  float finish = 0.f;
+  for (int x = 0; x < mbe::kXcds; ++x) {
+    const int first = std::min(len[x], kCusPerXcd);
+    float heap[kCusPerXcd];
+    float end = 0.f;
+    for (int j = 0; j < first; ++j) {
+      heap[j] = tiles[x][j] + static_cast<float>(kUnitStartTiles);
+      end = std::max(end, heap[j]);
+    }
+    if (len[x] > kCusPerXcd) {
+      std::make_heap(heap, heap + kCusPerXcd, std::greater<float>());
+      for (int j = kCusPerXcd; j < len[x]; ++j) {
+        std::pop_heap(heap, heap + kCusPerXcd, std::greater<float>());
+        const float t = heap[kCusPerXcd - 1] + tiles[x][j] + static_cast<float>(kUnitStartTiles);
+        heap[kCusPerXcd - 1] = t;
+        std::push_heap(heap, heap + kCusPerXcd, std::greater<float>());
+        end = std::max(end, t);
+      }
+    }
+    finish = std::max(finish, end);
+  }
+  if (any_split) finish += static_cast<float>(kMergeStartTiles + merge_bytes / kMergeBytesPerTile);
+  int slots = 0;
+  for (int x = 0; x < mbe::kXcds; ++x) slots = std::max(slots, len[x]);
+  out->finish = finish;
+  out->order_n = slots * mbe::kXcds;
+  for (int j = 0; j < slots; ++j)
+    for (int x = 0; x < mbe::kXcds; ++x) out->order[j * mbe::kXcds + x] = j < len[x] ? unit[x][j] : mbe::kNoUnit;
+}
 
 mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_t block_size,
                           int32_t window_bound, int32_t fixed_window, AttnPlan *pl) {
@@ -94,7 +235,7 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
 
   // Host copies of the lengths, when given, refine the plan.
   const bool host = o->host_prefix_lens && (fixed_window >= 0 || o->host_window_lens) &&
-                    o->batch > 0 && o->batch <= mbe::kMaxOrderedSeqs;
+                    o->batch > 0 && o->batch <= mbe::kMaxOrder;
   std::vector<int64_t> n_seq;   // keys each sequence's units read
   if (host) {
     n_seq.resize(o->batch);
@@ -109,6 +250,7 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   }
 
   int64_t chunk = o->kv_split_tokens;
+  bool rule_split = false;      // the default rule below cut the key ranges to fill the CUs
   if (chunk == 0) {
     // Work units (sequence, KV head, query tile, split) with splits of c keys.
     auto units = [&](int64_t c) {
@@ -142,20 +284,58 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
         else lo = mid + 1;
       }
       chunk = lo * mbe::kKeyTile;
+      rule_split = true;
     }
   }
   chunk = std::max<int64_t>(mbe::kKeyTile, (chunk + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
+
+  // Ragged small batches (the rule above split them, and the lengths
+  // differ): a dispatch table that balances the units over the XCDs and CUs,
+  // for the default split length or 7/8 or 3/4 of it, whichever the model
+  // finishes first (the default unless another beats it by kMinPlanGain).
+  // Equal lengths are balanced by the formula already, and large batches
+  // gained nothing from a table.
+  UnitSchedule sched;
+  if (host && rule_split) {
+    bool ragged = false;
+    for (int b = 1; b < o->batch; ++b) ragged = ragged || n_seq[b] != n_seq[0];
+    if (ragged) {
+      std::vector<SeqWork> seqs(o->batch);
+      for (int b = 0; b < o->batch; ++b) {
+        const int64_t W = fixed_window >= 0 ? fixed_window : o->host_window_lens[b];
+        seqs[b] = {n_seq[b], W, static_cast<int32_t>((pl->group * W + mbe::kRowsPerTile - 1) / mbe::kRowsPerTile)};
+      }
+      schedule_units(seqs, kv->num_kv_heads, pl->qtiles, o->num_q_heads, kv->head_dim, max_kv, chunk, &sched);
+      UnitSchedule alt;
+      const int64_t d = chunk;
+      for (int64_t cand : {d * 7 / 8, d * 3 / 4}) {
+        const int64_t c = std::max<int64_t>(kMinChunk, (cand + mbe::kKeyTile - 1) / mbe::kKeyTile * mbe::kKeyTile);
+        if (c >= d) continue;
+        schedule_units(seqs, kv->num_kv_heads, pl->qtiles, o->num_q_heads, kv->head_dim, max_kv, c, &alt);
+        if (alt.finish >= 0 && (sched.finish < 0 || alt.finish < sched.finish * (1.0 - kMinPlanGain))) {
+          chunk = c;
+          sched = alt;
+        }
+      }
+    }
+  }
+
   pl->kv_chunk = static_cast<int32_t>(std::min<int64_t>(chunk, 1LL << 30));
   pl->splits = static_cast<int32_t>(std::max<int64_t>(1, (max_kv + chunk - 1) / chunk));
   pl->groups = static_cast<int64_t>(o->batch) * kv->num_kv_heads * pl->splits;
   pl->slots_per_xcd = (pl->groups + mbe::kXcds - 1) / mbe::kXcds * pl->qtiles;
   if (pl->slots_per_xcd * mbe::kXcds > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "grid too large");
 
-  // Longest sequences first (stable), so the short ones fill in at the end.
-  // (no table when that is the natural order, e.g. one sequence or equal
-  // lengths: the kernel then skips reading it)
+  pl->order_kind = mbe::kOrderNone;
   pl->order_n = 0;
-  if (host) {
+  if (sched.finish >= 0) {
+    pl->order_kind = mbe::kOrderUnits;
+    pl->order_n = sched.order_n;
+    std::copy(sched.order, sched.order + sched.order_n, pl->order);
+  } else if (host) {
+    // Longest sequences first (stable), so the short ones fill in at the end
+    // (no table when that is the natural order, e.g. one sequence or equal
+    // lengths: the kernel then skips reading it).
     std::vector<int32_t> idx(o->batch);
     for (int b = 0; b < o->batch; ++b) idx[b] = b;
     std::stable_sort(idx.begin(), idx.end(), [&](int32_t x, int32_t y) { return n_seq[x] > n_seq[y]; });
@@ -164,7 +344,10 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
       pl->order[b] = static_cast<uint16_t>(idx[b]);
       natural = natural && idx[b] == b;
     }
-    pl->order_n = natural ? 0 : o->batch;
+    if (!natural) {
+      pl->order_kind = mbe::kOrderSeqs;
+      pl->order_n = o->batch;
+    }
   }
 
   pl->bytes = 0;
@@ -280,8 +463,9 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   p.kv_chunk = pl.kv_chunk;
   p.groups = pl.groups;
   p.slots_per_xcd = pl.slots_per_xcd;
-  p.seq_order_n = pl.order_n;
-  for (int i = 0; i < pl.order_n; ++i) p.seq_order[i] = pl.order[i];
+  p.order_kind = pl.order_kind;
+  p.order_n = pl.order_n;
+  for (int i = 0; i < pl.order_n; ++i) p.order[i] = pl.order[i];
   const float scale = o->softmax_scale > 0.f ? o->softmax_scale : 1.0f / std::sqrt(static_cast<float>(kv->head_dim));
   p.scale_log2 = scale * 1.4426950408889634f;
   const int mode = fixed_window >= 0 ? MBE_MASK_WINDOW_BIDIR : o->mask_mode;

@@ -210,23 +210,34 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   __shared__ __align__(1024) char lds2[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds3[Tile<D>::kBufBytes];
 
-  // ---- work unit.  Groups (split, sequence rank, KV head), split slowest,
-  // are dealt to the XCDs round-robin in dispatch order (workgroup id % 8 is
-  // the XCD), and the qtiles query tiles of a group, which read the same keys,
-  // take consecutive slots of the same XCD so that the second finds the keys
-  // in that XCD's L2.  With the split slowest every XCD gets the same mix of
-  // first and later splits (later splits of short sequences have no work).
+  // ---- work unit.  Workgroup id % 8 is the XCD that runs it.  With a
+  // dispatch table the host has placed every unit (groups dealt largest
+  // first to the least-loaded XCD, each XCD's longest units first).
+  // Otherwise groups (split, sequence rank, KV head), split slowest, are dealt
+  // to the XCDs round-robin, so that every XCD gets the same mix of first and
+  // later splits (later splits of short sequences have no work).  Either way
+  // the qtiles query tiles of a group, which read the same keys, take
+  // consecutive slots of one XCD so that the second finds the keys in its L2.
   const int64_t id = blockIdx.x;
-  const int64_t slot = id / kXcds;
-  const int64_t grp = (slot / p.qtiles) * kXcds + id % kXcds;
-  if (grp >= p.groups) return;
-  const int qtile = static_cast<int>(slot % p.qtiles);
+  int64_t grp;
+  int qtile;
+  if (p.order_kind == kOrderUnits) {
+    const int u = p.order[id];             // the grid has order_n workgroups
+    if (u == kNoUnit) return;
+    grp = u / p.qtiles;
+    qtile = u % p.qtiles;
+  } else {
+    const int64_t slot = id / kXcds;
+    grp = (slot / p.qtiles) * kXcds + id % kXcds;
+    if (grp >= p.groups) return;
+    qtile = static_cast<int>(slot % p.qtiles);
+  }
   const int64_t per_split = static_cast<int64_t>(p.batch) * p.num_kv_heads;
   const int split = static_cast<int>(grp / per_split);
   const int64_t rg = grp % per_split;
   const int rank = static_cast<int>(rg / p.num_kv_heads);
   const int g = static_cast<int>(rg % p.num_kv_heads);
-  const int b = rank < p.seq_order_n ? p.seq_order[rank] : rank;
+  const int b = (p.order_kind == kOrderSeqs && rank < p.order_n) ? p.order[rank] : rank;
 
   const int G = p.group;
   const int tid = threadIdx.x;
@@ -732,7 +743,7 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
 
 template <int D, int MODE>
 hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
-  const int64_t grid = p.slots_per_xcd * kXcds;
+  const int64_t grid = p.order_kind == kOrderUnits ? p.order_n : p.slots_per_xcd * kXcds;
   if (p.key_split == 2)
     hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
                        stream, p);

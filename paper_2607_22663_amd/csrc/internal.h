@@ -15,9 +15,12 @@ constexpr int kRowsPerWave = 64;      // packed (window position, q head) rows p
 constexpr int kWaves = 4;
 constexpr int kRowsPerTile = kRowsPerWave * kWaves;   // rows per workgroup
 constexpr int kXcds = 8;              // MI355X: workgroups go round-robin over 8 XCDs
-constexpr int kMaxOrderedSeqs = 1024; // dispatch order passed in the kernel arguments
+constexpr int kMaxOrder = 1024;       // dispatch-order entries passed in the kernel arguments
+constexpr uint16_t kNoUnit = 0xFFFF;  // dispatch-table slot without work
 
 
+
+enum AttnOrderKind : int32_t { kOrderNone = 0, kOrderSeqs = 1, kOrderUnits = 2 };
 
 struct AttnParams {
   const uint16_t *q;          // bf16 [total_q][Hq][D]
@@ -37,10 +40,16 @@ struct AttnParams {
   int64_t groups;             // (split, sequence rank, KV head) groups of qtiles work units
   int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
-  // Sequences in the order their work is dispatched (longest first), when the
-  // host knows the lengths; seq_order_n == 0 means natural order.
-  int32_t seq_order_n;
-  uint16_t seq_order[kMaxOrderedSeqs];
+  // Dispatch order, from the host lengths when given.
+  //   kOrderSeqs:  order[rank] is the sequence of that rank (longest first);
+  //                groups are dealt round-robin to the XCDs by formula.
+  //   kOrderUnits: workgroup i < order_n runs work unit order[i] =
+  //                grp * qtiles + query tile (kNoUnit: none), where
+  //                grp = split * batch * Hkv + sequence * Hkv + KV head.
+  //   kOrderNone:  natural sequence order, formula dealing.
+  int32_t order_kind;
+  int32_t order_n;
+  uint16_t order[kMaxOrder];
 };
 
 hipError_t launch_window_attention(const AttnParams &p, int head_dim, int mask_mode,
