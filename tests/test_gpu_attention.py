@@ -398,3 +398,15 @@ def test_pool_beyond_2_31_elements(gpu):
     assert np.array_equal(V[idx].cpu().view(torch.int16).numpy(), rv)
     del K, V
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_dispatch_table_ragged_windows(gpu, mode):
+    """A small ragged batch with host lengths takes the host-placed dispatch
+    table; with 8 query heads per KV head and windows of 1 to 4 blocks the
+    sequences have 1 or 2 query tiles, the table's general ordering path."""
+    spec = synth.AttnSpec(5, 16, 4, ("fixed", 0), 16, 2, 64)
+    case = synth.make_attention_case(spec, 57, prefix_lens=[100, 3000, 700, 1500, 50],
+                                     window_lens=[16, 64, 32, 48, 0], tail_fill=float("nan"))
+    out = run_case(gpu, case, mode, host_prefix_lens=case.prefix_lens, host_window_lens=case.window_lens)
+    assert_attn_close(out, oracle_case(case, mode), f"dispatch table, ragged windows, {mode}")
