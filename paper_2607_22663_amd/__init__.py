@@ -163,6 +163,34 @@ def _workspace(kind: str, device: torch.device, nbytes: int) -> Optional[torch.T
     return ws
 
 
+MBE_ERR_WORKSPACE = 4
+
+
+def _call_with_workspace(call, size, opts, device, workspace):
+    """Runs an attention call whose split plan may need a workspace.  With a
+    caller's workspace, that one.  Otherwise the shared workspace of this
+    stream as it is, first: only when the library reports it too small (or
+    absent) is the size queried, the workspace grown and the call repeated, so
+    a steady stream of calls plans once per call."""
+    if workspace is not None:
+        if workspace.dtype != torch.uint8 or not workspace.is_cuda:
+            raise ValueError("workspace must be a uint8 device tensor")
+        opts.workspace, opts.workspace_bytes = _ptr(workspace), workspace.numel()
+        return call()
+    key = ("attn", device.index, torch.cuda.current_stream(device).cuda_stream)
+    ws = _workspaces.get(key)
+    opts.workspace, opts.workspace_bytes = (_ptr(ws), ws.numel()) if ws is not None else (None, 0)
+    status = call()
+    if status != MBE_ERR_WORKSPACE:
+        return status
+    need = size()
+    if need == ctypes.c_size_t(-1).value:
+        return status
+    ws = _workspace("attn", device, need)
+    opts.workspace, opts.workspace_bytes = (_ptr(ws), need) if ws is not None else (None, 0)
+    return call()
+
+
 def _own_workspace(ws: torch.Tensor, need: int) -> Optional[torch.Tensor]:
     if need == 0:
         return None
@@ -263,16 +291,14 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(max_window_len), MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode),
                     float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), _ptr(hw), None, 0, stream)
-    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
-    if need == ctypes.c_size_t(-1).value:
-        _check("mbe_window_attention", lib.mbe_window_attention(
-            None, ctypes.byref(kv), None, None, None, int(block_size), None, ctypes.byref(opts)))
-    ws = _workspace("attn", q.device, need) if workspace is None else _own_workspace(workspace, need)
-    opts.workspace = _ptr(ws)
-    opts.workspace_bytes = need
-    _check("mbe_window_attention", lib.mbe_window_attention(
-        _ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens), _ptr(window_lens),
-        int(block_size), _ptr(out), ctypes.byref(opts)))
+    def call():
+        return lib.mbe_window_attention(_ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens),
+                                        _ptr(window_lens), int(block_size), _ptr(out), ctypes.byref(opts))
+
+    def size():
+        return lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+
+    _check("mbe_window_attention", _call_with_workspace(call, size, opts, q.device, workspace))
     return out
 
 
@@ -294,16 +320,14 @@ def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, bloc
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), None,
                     None, 0, stream)
-    need = lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
-    if need == ctypes.c_size_t(-1).value:
-        _check("block_diffusion_attention", lib.block_diffusion_attention(
-            None, ctypes.byref(kv), None, None, int(block_size), None, ctypes.byref(opts)))
-    ws = _workspace("attn", q.device, need)
-    opts.workspace = _ptr(ws)
-    opts.workspace_bytes = need
-    _check("block_diffusion_attention", lib.block_diffusion_attention(
-        _ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens), int(block_size), _ptr(out),
-        ctypes.byref(opts)))
+    def call():
+        return lib.block_diffusion_attention(_ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens),
+                                             int(block_size), _ptr(out), ctypes.byref(opts))
+
+    def size():
+        return lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+
+    _check("block_diffusion_attention", _call_with_workspace(call, size, opts, q.device, None))
     return out
 
 
