@@ -8,7 +8,9 @@ restores a cache consistent with standard-scope decoding.
 kv_write is the write-back: token t of sequence b (absolute position
 start_b + t, t < n_b) goes to slot (start_b + t) % 16 of page
 page_table[b][(start_b + t) // 16], for every KV head.  The K pool is
-[page][head][16][D]; the V pool [page][head][D][16] (token-minor).
+[page][head][16][D]; the V pool [page][head][D][16] (token-minor).  With
+block flags ([batch][blocks], block size B), token t of sequence b is
+written only when flags[b][t // B] is set: the blocks the refresh recomputes.
 
 refresh_blocks reads which blocks to recompute from the per-block changed
 flags.  The paper refreshes only the changed blocks; because a later block's
@@ -27,7 +29,7 @@ def _np(x):
     return x.detach().cpu().numpy() if hasattr(x, "detach") else np.asarray(x)
 
 
-def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new):
+def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, block_flags=None, block_size=None):
     """Returns updated copies of the two pools (same dtype as given)."""
     K = _np(k_pages).copy()
     V = _np(v_pages).copy()
@@ -36,14 +38,16 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new):
     n = _np(lens).astype(np.int64)
     kn = _np(k_new)
     vn = _np(v_new)
+    fl = None if block_flags is None else _np(block_flags)
     row = 0
     for b in range(st.shape[0]):
         for t in range(int(n[b])):
-            pos = int(st[b]) + t
-            page = int(pt[b, pos // PAGE])
-            slot = pos % PAGE
-            K[page, :, slot, :] = kn[row]
-            V[page, :, :, slot] = vn[row]
+            if fl is None or fl[b, t // int(block_size)]:
+                pos = int(st[b]) + t
+                page = int(pt[b, pos // PAGE])
+                slot = pos % PAGE
+                K[page, :, slot, :] = kn[row]
+                V[page, :, :, slot] = vn[row]
             row += 1
     return K, V
 

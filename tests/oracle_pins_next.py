@@ -15,8 +15,14 @@ Entropy and tail selection (Eqs. (3), (5), (6)):
   rows; invariance to a constant shift; tail scores by repeated removal of the
   maximum; start block by scanning candidates in a different order.
 KV write:
+  hand-derived fixture (tests/golden/kv_write_hand.json: the page and slot of
+  every written row, with and without block flags, worked out by hand);
   read-back through an independent gather loop equals the written values and
-  every other slot is untouched; refresh modes by a direct definition.
+  every other slot is untouched; round trip: contiguous K/V written into
+  shuffled, NaN-filled pages (prefix and window in separate writes, the
+  window starting mid-page) and read by the brute-force attention give the
+  mean of the written V rows for q = 0 and torch's fp64 SDPA over the
+  contiguous K/V for random q; refresh modes by a direct definition.
 """
 from __future__ import annotations
 
@@ -238,4 +244,85 @@ def check_refresh_modes(kv):
     assert np.array_equal(kv.refresh_blocks(C, 1), want)
 
 
-KV_CHECKS = [check_kv_write, check_refresh_modes]
+def check_kv_write_golden(kv):
+    """Every row lands on the (page, slot) the fixture gives; nothing else
+    changes.  Markers: K row r of head g = (r + 1) * 10 + g in every dim, V
+    row r = -(that)."""
+    fx = _fixture("kv_write_hand.json")
+    npg, H, D = fx["num_pages"], fx["num_kv_heads"], fx["head_dim"]
+    rows = int(sum(fx["lens"]))
+    kn = np.array([[[(r + 1) * 10.0 + g] * D for g in range(H)] for r in range(rows)])
+    vn = -kn
+    for flags, want in ((None, fx["written_row_page_slot"]), (fx["block_flags"], fx["written_with_flags"])):
+        K0 = np.full((npg, H, 16, D), 0.5)
+        V0 = np.full((npg, H, D, 16), 0.5)
+        kw = {} if flags is None else {"block_flags": np.array(flags, dtype=np.uint8),
+                                        "block_size": fx["flags_block_size"]}
+        K, V = kv.kv_write(K0, V0, np.array(fx["page_table"]), np.array(fx["start_pos"]), np.array(fx["lens"]),
+                           kn, vn, **kw)
+        hit = np.zeros((npg, 16), dtype=bool)
+        for r, page, slot in want:
+            hit[page, slot] = True
+            for g in range(H):
+                assert np.all(K[page, g, slot, :] == kn[r, g]), (r, page, slot, K[page, g, slot])
+                assert np.all(V[page, g, :, slot] == vn[r, g]), (r, page, slot, V[page, g, :, slot])
+        for page in range(npg):
+            for slot in range(16):
+                if not hit[page, slot]:
+                    assert np.all(K[page, :, slot, :] == 0.5) and np.all(V[page, :, :, slot] == 0.5), (page, slot)
+
+
+def check_kv_write_round_trip(kv):
+    """Contiguous K/V of two sequences written into shuffled pages filled with
+    NaN, the prefix and the window in separate writes (the window starts
+    mid-page), then read back by the brute-force attention: q = 0 gives the
+    mean of the written V rows over the visible keys, random q gives torch's
+    fp64 SDPA over the contiguous K/V (block-id mask in block-causal mode)."""
+    import torch
+    import oracle
+    rng = np.random.default_rng(17)
+    Hkv, G, D, B = 2, 2, 4, 4
+    Hq = Hkv * G
+    P = np.array([21, 5])
+    W = np.array([8, 4])
+    n = P + W
+    npg = 9
+    perm = rng.permutation(npg)
+    need = (n + 15) // 16
+    pt = np.zeros((2, 2), dtype=np.int64)
+    pt[0, :need[0]] = perm[:need[0]]
+    pt[1, :need[1]] = perm[need[0]:need[0] + need[1]]
+    Kc = [rng.normal(size=(int(n[b]), Hkv, D)) for b in range(2)]
+    Vc = [rng.normal(size=(int(n[b]), Hkv, D)) for b in range(2)]
+    K = np.full((npg, Hkv, 16, D), np.nan)
+    V = np.full((npg, Hkv, D, 16), np.nan)
+    # prefix tokens of both sequences, then the windows from position P_b
+    K, V = kv.kv_write(K, V, pt, np.zeros(2, dtype=np.int64), P, np.concatenate([Kc[b][:P[b]] for b in range(2)]),
+                       np.concatenate([Vc[b][:P[b]] for b in range(2)]))
+    K, V = kv.kv_write(K, V, pt, P, W, np.concatenate([Kc[b][P[b]:] for b in range(2)]),
+                       np.concatenate([Vc[b][P[b]:] for b in range(2)]))
+    q0 = np.zeros((int(W.sum()), Hq, D))
+    out = np.array(oracle.brute_window_attention(q0, K, V, pt, P, W, B, bidirectional=True))
+    row = 0
+    for b in range(2):
+        for i in range(int(W[b])):
+            for h in range(Hq):
+                assert np.allclose(out[row + i, h], Vc[b][:, h // G].mean(axis=0), rtol=0, atol=1e-12)
+        row += int(W[b])
+    q = rng.normal(size=(int(W.sum()), Hq, D))
+    for bidir in (True, False):
+        out = np.array(oracle.brute_window_attention(q, K, V, pt, P, W, B, bidirectional=bidir))
+        row = 0
+        for b in range(2):
+            ids = np.concatenate([np.full(P[b], -1), np.arange(W[b]) // B])
+            allowed = torch.from_numpy(bidir | (ids[None, :] <= ids[P[b]:, None]))
+            for h in range(Hq):
+                qh = torch.from_numpy(q[row:row + W[b], h])[None]
+                kh = torch.from_numpy(Kc[b][:, h // G])[None]
+                vh = torch.from_numpy(Vc[b][:, h // G])[None]
+                ref = torch.nn.functional.scaled_dot_product_attention(qh, kh, vh, attn_mask=allowed)[0].numpy()
+                assert np.allclose(out[row:row + W[b], h], ref, rtol=0, atol=1e-12), (b, h, bidir)
+            row += int(W[b])
+
+
+KV_CHECKS = [check_kv_write_golden, check_kv_write, check_kv_write_round_trip, check_refresh_modes]

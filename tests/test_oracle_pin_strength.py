@@ -124,6 +124,15 @@ KV_MUTATIONS = {
     "slot off by one": ("slot = pos % PAGE", "slot = (pos + 1) % PAGE"),
     "positions relative to the page start": ("pos = int(st[b]) + t", "pos = t"),
     "later-block mode refreshes nothing extra": ("elif seen and mode == REFRESH_CHANGED_AND_LATER:", "elif False:"),
+    "page from the token index, not the position": ("page = int(pt[b, pos // PAGE])", "page = int(pt[b, t // PAGE])"),
+    "start offset off by one": ("pos = int(st[b]) + t", "pos = int(st[b]) + t + 1"),
+    "page stride of 8 tokens": ("page = int(pt[b, pos // PAGE])", "page = int(pt[b, min(pos // 8, pt.shape[1] - 1)])"),
+    "K and V rows swapped": ("K[page, :, slot, :] = kn[row]", "K[page, :, slot, :] = vn[row]"),
+    "block flags ignored": ("if fl is None or fl[b, t // int(block_size)]:", "if True:"),
+    "block flag of the absolute position": ("fl[b, t // int(block_size)]",
+                                            "fl[b, min((int(st[b]) + t) // int(block_size), fl.shape[1] - 1)]"),
+    "rows counted only when written": ("                V[page, :, :, slot] = vn[row]\n            row += 1",
+                                       "                V[page, :, :, slot] = vn[row]\n                row += 1"),
 }
 
 
