@@ -16,11 +16,13 @@
  *     check returns a non-OK status, launches nothing and writes nothing.
  *     mbe_last_error() then holds a thread-local description.
  *   - Per-sequence values that live in device memory (page ids, lengths) are
- *     preconditions and are not read back.  Page ids outside [0, num_pages)
- *     are clamped into range, so a bad table gives wrong numbers but never an
- *     out-of-bounds access.  With the environment variable MBE_DEBUG_CHECK=1,
- *     the attention calls copy the lengths and the page table to the host
- *     (on the call's stream, then synchronising it) and return
+ *     preconditions and are not read back.  The attention calls clamp page
+ *     ids outside [0, num_pages) into range, so a bad table gives wrong
+ *     numbers but never an out-of-bounds access; the KV write-back skips a
+ *     token whose table slot or page id is out of range instead of writing
+ *     it anywhere else.  With the environment variable MBE_DEBUG_CHECK=1, the
+ *     attention calls and mbe_kv_write copy the lengths and the page table to
+ *     the host (on the call's stream, then synchronising it) and return
  *     MBE_ERR_BAD_VALUE on a violation; calls made while the stream is being
  *     captured into a graph are not checked.
  *   - An error from the HIP runtime is returned as MBE_ERR_HIP, with the HIP
@@ -109,6 +111,24 @@ typedef struct {
                                  when that size is 0                                 */
   size_t workspace_bytes;
   void *stream;               /* hipStream_t                                        */
+  const uint8_t *block_flags; /* optional DEVICE uint8 [batch][max_window_len /
+                                 block_size] (NULL = every row).  The rows of window
+                                 block i of sequence b (positions i*B .. i*B+B-1)
+                                 are computed and written only when
+                                 block_flags[b * (max_window_len / block_size) + i]
+                                 is nonzero; the other rows of out are left as they
+                                 were.  This is the targeted refresh: recompute
+                                 only the blocks an editing pass changed (paper,
+                                 Sec. "Infrastructure Optimization", cache control).
+                                 block_diffusion_attention reads one flag per
+                                 sequence ([batch][1]).                             */
+  const int32_t *run_if_nonzero; /* optional DEVICE int32 (NULL = always run).  When
+                                 it holds 0 when the call runs on the stream, the
+                                 call computes and writes nothing.  With the changed
+                                 count of the previous editing pass, a sequence of
+                                 at most N_MBE passes captured in one graph stops
+                                 early without a host round trip (paper, Sec.
+                                 "Training-Free MBE Decoding", the pass loop).      */
 } mbe_attn_opts;
 
 /* Editing-window attention (paper, Sec. "Training-Free MBE Decoding", Eq. (4)).
@@ -197,16 +217,27 @@ size_t mbe_edit_select_workspace_size(int64_t rows, int64_t vocab);
  * copying per-row results to the host.  entropy (may be NULL) receives each
  * row's softmax entropy in nats, -sum_v p_v ln p_v, computed in the same pass
  * over the logits (the input of the tail-entropy selection below).
+ * run_if_nonzero (device int32, may be NULL): when it holds 0 the pass
+ * changes nothing without reading the logits: every action is MBE_KEEP,
+ * new_tokens = cur_tokens, block_changed = 0 and changed_count = 0, while
+ * conf and entropy are left as they were.  Given the previous pass's
+ * changed_count (a different buffer: the pass zeroes its own), the passes
+ * after the first one that changes nothing cost about a launch each, with no
+ * host read (paper, Sec. "Training-Free MBE Decoding": at most N_MBE passes,
+ * stopping when no token changes).  new_tokens may be cur_tokens itself (an
+ * in-place update).
  * rows must be a multiple of block_size.  logits/threshold contract as for
  * mbe_edit_select.  workspace: mbe_threshold_update_workspace_size bytes,
- * 256-byte aligned, any contents.  MBE_ERR_BAD_VALUE for a NaN threshold. */
+ * 256-byte aligned, any contents.  MBE_ERR_BAD_VALUE for a NaN threshold or
+ * run_if_nonzero == changed_count. */
 typedef enum { MBE_KEEP = 0, MBE_UNMASK = 1, MBE_FORCE_UNMASK = 2, MBE_EDIT = 3 } mbe_action;
 
 mbe_status mbe_threshold_update(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
                                 const int32_t *cur_tokens, int32_t mask_id, int32_t block_size,
                                 float omega_mask, float omega_edit, int32_t *new_tokens, float *conf,
                                 uint8_t *action, uint8_t *block_changed, int32_t *changed_count,
-                                float *entropy, void *workspace, size_t workspace_bytes, void *stream);
+                                float *entropy, const int32_t *run_if_nonzero, void *workspace,
+                                size_t workspace_bytes, void *stream);
 
 /* Workspace bytes mbe_threshold_update needs (the per-row predictions plus
  * the per-chunk partials of mbe_edit_select).  (size_t)-1 for negative sizes. */
@@ -239,12 +270,19 @@ mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t sc
  *   v_pages[page][head][:][slot] = v_new[row][head][:]      (token-minor pool)
  * k_new/v_new: bf16 [total_tokens][num_kv_heads][head_dim]; max_len bounds
  * every lens[b] (host-known, sizes the grid).  Other slots are not touched.
- * Positions must lie inside the sequence's page table row (a precondition;
- * page ids are clamped into the pool). */
+ * block_flags (device uint8, may be NULL = write every token): the targeted
+ * refresh; token t of sequence b is written only when
+ * block_flags[b * ceil(max_len / block_size) + t / block_size] is nonzero
+ * (the row numbering of k_new/v_new does not change).  block_size >= 1 when
+ * block_flags is given, ignored otherwise.
+ * Preconditions (checked under MBE_DEBUG_CHECK=1): positions lie inside the
+ * sequence's table row, page ids inside the pool, sum of lens = total_tokens.
+ * A token that breaks them is not written (it never lands on another slot). */
 mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads,
                         int32_t head_dim, const int32_t *page_table, int32_t max_pages_per_seq,
                         const int32_t *start_pos, const int32_t *lens, int32_t batch, int32_t max_len,
-                        int32_t total_tokens, const void *k_new, const void *v_new, void *stream);
+                        int32_t total_tokens, const void *k_new, const void *v_new,
+                        const uint8_t *block_flags, int32_t block_size, void *stream);
 
 /* Blocks to recompute after editing, from the per-block changed flags
  * ([batch][num_blocks], e.g. block_changed of mbe_threshold_update laid out

@@ -53,7 +53,8 @@ class AttnOpts(ctypes.Structure):
                 ("mask_mode", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
                 ("kv_split_tokens", ctypes.c_int32), ("host_prefix_lens", ctypes.c_void_p),
                 ("host_window_lens", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
-                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p)]
+                ("workspace_bytes", ctypes.c_size_t), ("stream", ctypes.c_void_p),
+                ("block_flags", ctypes.c_void_p), ("run_if_nonzero", ctypes.c_void_p)]
 
 
 _lib = None
@@ -91,7 +92,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_edit_select_workspace_size.restype = sz
         f32 = ctypes.c_float
         lib.mbe_threshold_update.argtypes = [vp, i64, i64, i64, vp, i32, i32, f32, f32, vp, vp, vp, vp, vp, vp, vp,
-                                             sz, vp]
+                                             vp, sz, vp]
         lib.mbe_threshold_update.restype = ctypes.c_int
         lib.mbe_threshold_update_workspace_size.argtypes = [i64, i64]
         lib.mbe_threshold_update_workspace_size.restype = sz
@@ -99,7 +100,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_tail_entropy_scores.restype = ctypes.c_int
         lib.mbe_select_start_block.argtypes = [vp, i32, i32, vp, i32, vp, vp]
         lib.mbe_select_start_block.restype = ctypes.c_int
-        lib.mbe_kv_write.argtypes = [vp, vp, i32, i32, i32, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp]
+        lib.mbe_kv_write.argtypes = [vp, vp, i32, i32, i32, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp]
         lib.mbe_kv_write.restype = ctypes.c_int
         lib.mbe_refresh_blocks.argtypes = [vp, i32, i32, i32, vp, vp]
         lib.mbe_refresh_blocks.restype = ctypes.c_int
@@ -212,7 +213,7 @@ def workspace_bytes_window_attention(q, k_pages, page_table, batch, block_size, 
     kv = PagedKV(None, None, k_pages.shape[0], k_pages.shape[2], k_pages.shape[1], k_pages.shape[3])
     opts = AttnOpts(int(batch), q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len), int(max_window_len),
                     MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode), 0.0,
-                    int(kv_split_tokens), None, None, None, 0, None)
+                    int(kv_split_tokens), None, None, None, 0, None, None, None)
     n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
     if n == ctypes.c_size_t(-1).value:
         raise ValueError("invalid attention shapes")
@@ -248,6 +249,17 @@ def _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out):
     return kv, out
 
 
+def _flags_gate(block_flags, shape, gate, device):
+    if block_flags is not None:
+        _need(block_flags, "block_flags", torch.uint8, device, 2)
+        if tuple(block_flags.shape) != tuple(shape):
+            raise ValueError(f"block_flags must be {tuple(shape)}, got {tuple(block_flags.shape)}")
+    if gate is not None:
+        _need(gate, "run_if_nonzero", torch.int32, device)
+        if gate.numel() < 1:
+            raise ValueError("run_if_nonzero must hold one int32")
+
+
 def _host_i32(x, batch, name):
     """A contiguous host int32 copy (kept alive by the caller) or None."""
     if x is None:
@@ -262,7 +274,7 @@ def _host_i32(x, batch, name):
 def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, block_size, *,
                      out=None, mask_mode="bidir", softmax_scale=None, max_prefix_len=None,
                      max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None,
-                     workspace=None):
+                     workspace=None, block_flags=None, run_if_nonzero=None):
     """MBE editing-window attention (paper, Sec. "Training-Free MBE Decoding",
     Eq. (4)).  Layouts as in include/mbe.h.
 
@@ -272,7 +284,11 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     When neither bounds nor host lengths are given, the lengths are copied
     from the device (a synchronisation).  workspace: an optional caller-owned
     uint8 device tensor used instead of the module's shared one (as a
-    captured graph needs)."""
+    captured graph needs).  block_flags: optional uint8 [batch,
+    max_window_len / block_size] device tensor; only the rows of flagged
+    window blocks are computed and written (targeted refresh).
+    run_if_nonzero: optional int32 [1] device tensor; the call does nothing
+    when it holds 0 (e.g. the previous editing pass's changed count)."""
     lib = load()
     kv, out = _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out)
     _need(window_lens, "window_lens", torch.int32, q.device, 1)
@@ -288,9 +304,12 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
     if max_window_len is None:
         max_window_len = int(hw.max()) if batch else 0
     stream = _stream(q.device)
+    nblk = int(max_window_len) // int(block_size) if int(block_size) > 0 else 0
+    _flags_gate(block_flags, (batch, nblk), run_if_nonzero, q.device)
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(max_window_len), MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode),
-                    float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), _ptr(hw), None, 0, stream)
+                    float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), _ptr(hw), None, 0, stream,
+                    _ptr(block_flags), _ptr(run_if_nonzero))
     def call():
         return lib.mbe_window_attention(_ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens),
                                         _ptr(window_lens), int(block_size), _ptr(out), ctypes.byref(opts))
@@ -305,7 +324,7 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
 @_on_device
 def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size, *,
                               out=None, softmax_scale=None, max_prefix_len=None, kv_split_tokens=0,
-                              host_prefix_lens=None):
+                              host_prefix_lens=None, block_flags=None, run_if_nonzero=None):
     """Standard single-block step (paper, Sec. "Block diffusion"): q holds
     block_size rows per sequence."""
     lib = load()
@@ -317,9 +336,10 @@ def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, bloc
     if max_prefix_len is None:
         max_prefix_len = int(hp.max()) if batch else 0
     stream = _stream(q.device)
+    _flags_gate(block_flags, (batch, 1), run_if_nonzero, q.device)
     opts = AttnOpts(batch, q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len),
                     int(block_size), 0, float(softmax_scale or 0.0), int(kv_split_tokens), _ptr(hp), None,
-                    None, 0, stream)
+                    None, 0, stream, _ptr(block_flags), _ptr(run_if_nonzero))
     def call():
         return lib.block_diffusion_attention(_ptr(q), ctypes.byref(kv), _ptr(page_table), _ptr(prefix_lens),
                                              int(block_size), _ptr(out), ctypes.byref(opts))
@@ -365,12 +385,14 @@ def edit_select(logits, cur_tokens, threshold, *, vocab=None, out=None):
 
 @_on_device
 def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_edit, *, vocab=None,
-                     with_entropy=False, out=None, workspace=None):
+                     with_entropy=False, out=None, workspace=None, run_if_nonzero=None):
     """Full threshold update (paper, Eq. (1) with force-unmask).  Rows form
     blocks of block_size consecutive rows.  Returns a dict of device tensors:
     new_tokens int32, conf float32, action uint8 (ACTIONS), block_changed
     uint8 [rows / block_size], changed_count int32 [1] and, when asked,
-    entropy float32 (nats)."""
+    entropy float32 (nats).  out["new_tokens"] may be cur_tokens itself (in
+    place).  run_if_nonzero: optional int32 device tensor (not
+    out["changed_count"]); when it holds 0 the pass keeps every row."""
     lib = load()
     dev = logits.device
     _need(cur_tokens, "cur_tokens", torch.int32, dev, 1)
@@ -395,11 +417,12 @@ def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_
     need = lib.mbe_threshold_update_workspace_size(rows, v)
     need = need if need != ctypes.c_size_t(-1).value else 0
     ws = _workspace("update", dev, need) if workspace is None else _own_workspace(workspace, need)
+    _flags_gate(None, None, run_if_nonzero, dev)
     _check("mbe_threshold_update", lib.mbe_threshold_update(
         _ptr(logits), rows, v, ld, _ptr(cur_tokens), int(mask_id), int(block_size), ctypes.c_float(omega_mask),
         ctypes.c_float(omega_edit), _ptr(out["new_tokens"]), _ptr(out["conf"]), _ptr(out["action"]),
-        _ptr(out["block_changed"]), _ptr(out.get("changed_count")), _ptr(out.get("entropy")), _ptr(ws),
-        need if ws is not None else 0, _stream(dev)))
+        _ptr(out["block_changed"]), _ptr(out.get("changed_count")), _ptr(out.get("entropy")), _ptr(run_if_nonzero),
+        _ptr(ws), need if ws is not None else 0, _stream(dev)))
     return out
 
 
@@ -433,9 +456,12 @@ def select_start_block(scores, current_block, k_max, *, out=None):
 
 
 @_on_device
-def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max_len=None):
+def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max_len=None, block_flags=None,
+             block_size=None):
     """Write recomputed K/V (bf16 [total_tokens, heads, D]) into the paged
-    pools in place: token t of sequence b goes to position start_pos[b] + t."""
+    pools in place: token t of sequence b goes to position start_pos[b] + t.
+    block_flags: optional uint8 [batch, ceil(max_len / block_size)] device
+    tensor; only tokens of flagged blocks (t // block_size) are written."""
     lib = load()
     dev = k_pages.device
     _need(k_pages, "k_pages", torch.bfloat16, dev, 4)
@@ -448,10 +474,14 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max
     batch = start_pos.shape[0]
     if max_len is None:
         max_len = int(lens.max().item()) if batch else 0
+    if block_flags is not None:
+        if block_size is None or int(block_size) < 1:
+            raise ValueError("block_flags needs block_size >= 1")
+        _flags_gate(block_flags, (batch, -(-int(max_len) // int(block_size))), None, dev)
     _check("mbe_kv_write", lib.mbe_kv_write(
         _ptr(k_pages), _ptr(v_pages), k_pages.shape[0], k_pages.shape[1], k_pages.shape[3], _ptr(page_table),
         page_table.shape[1], _ptr(start_pos), _ptr(lens), batch, int(max_len), k_new.shape[0], _ptr(k_new),
-        _ptr(v_new), _stream(dev)))
+        _ptr(v_new), _ptr(block_flags), int(block_size or 0), _stream(dev)))
 
 
 @_on_device

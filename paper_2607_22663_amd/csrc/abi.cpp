@@ -404,6 +404,45 @@ mbe_status debug_check_attention(const mbe_paged_kv *kv, const int32_t *page_tab
   return MBE_OK;
 }
 
+// MBE_DEBUG_CHECK for the KV write-back: every written position must lie in
+// its sequence's table row and its page id in the pool, and the lengths must
+// fit the bounds and the rows of the input.
+mbe_status debug_check_kv_write(const int32_t *page_table, int32_t max_pages, int32_t num_pages,
+                                const int32_t *start_pos, const int32_t *lens, int32_t batch, int32_t max_len,
+                                int32_t total_tokens, hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return hip_fail(e, "MBE_DEBUG_CHECK capture query");
+  if (cs != hipStreamCaptureStatusNone) return MBE_OK;
+  std::vector<int32_t> S(batch), L(batch), T(static_cast<size_t>(batch) * max_pages);
+  e = hipMemcpyAsync(S.data(), start_pos, batch * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(L.data(), lens, batch * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(T.data(), page_table, T.size() * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "MBE_DEBUG_CHECK copy");
+  int64_t rows = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (L[b] < 0 || L[b] > max_len) return fail(MBE_ERR_BAD_VALUE, "lens[%d] = %d outside [0, %d]", b, L[b], max_len);
+    if (S[b] < 0) return fail(MBE_ERR_BAD_VALUE, "start_pos[%d] = %d < 0", b, S[b]);
+    rows += L[b];
+    if (L[b] == 0) continue;
+    const int64_t last = (static_cast<int64_t>(S[b]) + L[b] - 1) / mbe::kPageSize;
+    if (last >= max_pages)
+      return fail(MBE_ERR_BAD_VALUE, "sequence %d writes up to position %lld, past its %d table pages", b,
+                  static_cast<long long>(S[b]) + L[b] - 1, max_pages);
+    for (int64_t j = S[b] / mbe::kPageSize; j <= last; ++j) {
+      const int32_t pg = T[static_cast<size_t>(b) * max_pages + j];
+      if (pg < 0 || pg >= num_pages)
+        return fail(MBE_ERR_BAD_VALUE, "page_table[%d][%lld] = %d outside [0, %d)", b, static_cast<long long>(j), pg,
+                    num_pages);
+    }
+  }
+  if (rows != total_tokens)
+    return fail(MBE_ERR_BAD_VALUE, "sum of lens %lld != total_tokens %d", static_cast<long long>(rows), total_tokens);
+  return MBE_OK;
+}
+
 mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *page_table,
                          const int32_t *prefix_lens, const int32_t *window_lens, int32_t block_size,
                          int32_t fixed_window, void *out, const mbe_attn_opts *o) {
@@ -468,6 +507,9 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   for (int i = 0; i < pl.order_n; ++i) p.order[i] = pl.order[i];
   const float scale = o->softmax_scale > 0.f ? o->softmax_scale : 1.0f / std::sqrt(static_cast<float>(kv->head_dim));
   p.scale_log2 = scale * 1.4426950408889634f;
+  p.block_flags = o->block_flags;
+  p.flag_stride = window_bound / block_size;
+  p.gate = o->run_if_nonzero;
   const int mode = fixed_window >= 0 ? MBE_MASK_WINDOW_BIDIR : o->mask_mode;
   hipError_t e = mbe::launch_window_attention(p, kv->head_dim, mode, static_cast<hipStream_t>(o->stream));
   if (e != hipSuccess) return hip_fail(e, "window attention launch");
@@ -475,6 +517,110 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
 }
 
 }  // namespace
+
+namespace mbe {
+
+void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len) {
+  // Enough workgroups to cover the 256 CUs twice; a chunk keeps at least 4096
+  // elements, one full iteration of the workgroup.  (Measured on 64 rows of
+  // 131072: 512 workgroups of 4 iterations beat 2048 of one, whose time is
+  // dispatch and one memory round trip.)
+  const int64_t target_wgs = 512;
+  int64_t c = 1;
+  if (rows < target_wgs) {
+    c = (target_wgs + rows - 1) / rows;
+    const int64_t max_c = (vocab + 4095) / 4096;
+    if (c > max_c) c = max_c;
+    if (c > 1024) c = 1024;
+    if (c < 1) c = 1;
+  }
+  int64_t len = (vocab + c - 1) / c;
+  len = (len + 7) / 8 * 8;
+  c = (vocab + len - 1) / len;
+  if (c < 1) c = 1;
+  *chunks = static_cast<int32_t>(c);
+  *chunk_len = len;
+}
+
+mbe_status report(mbe_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+mbe_status threshold_update_check(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                  const int32_t *cur_tokens, int32_t block_size, float omega_mask, float omega_edit,
+                                  const int32_t *new_tokens, const float *conf, const uint8_t *action,
+                                  const uint8_t *block_changed, const int32_t *changed_count,
+                                  const int32_t *run_if_nonzero, size_t *need) {
+  *need = 0;
+  if (rows < 0 || vocab < 0) return fail(MBE_ERR_BAD_SHAPE, "rows %lld / vocab %lld negative",
+                                         static_cast<long long>(rows), static_cast<long long>(vocab));
+  if (rows > 0 && vocab < 1) return fail(MBE_ERR_BAD_SHAPE, "vocab must be >= 1");
+  if (row_stride < vocab)
+    return fail(MBE_ERR_BAD_SHAPE, "row_stride %lld < vocab %lld", static_cast<long long>(row_stride),
+                static_cast<long long>(vocab));
+  if (vocab > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "vocab beyond int32 indices");
+  if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
+  if (rows % block_size != 0)
+    return fail(MBE_ERR_BAD_SHAPE, "rows %lld is not a multiple of block_size %d", static_cast<long long>(rows),
+                block_size);
+  if (omega_mask != omega_mask || omega_edit != omega_edit) return fail(MBE_ERR_BAD_VALUE, "threshold is NaN");
+  if (run_if_nonzero && run_if_nonzero == changed_count)
+    return fail(MBE_ERR_BAD_VALUE, "run_if_nonzero must not be changed_count itself (the pass zeroes it)");
+  if (rows == 0) return MBE_OK;
+  if (!logits || !cur_tokens || !new_tokens || !conf || !action || !block_changed)
+    return fail(MBE_ERR_NULL_ARG, "logits, cur_tokens, new_tokens, conf, action and block_changed must be non-NULL");
+  int32_t chunks;
+  int64_t len;
+  edit_select_plan(rows, vocab, &chunks, &len);
+  if (rows * chunks > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "too many rows");
+  *need = mbe_threshold_update_workspace_size(rows, vocab);
+  return MBE_OK;
+}
+
+mbe_status threshold_update_launch(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                   const int32_t *cur_tokens, int32_t mask_id, int32_t block_size, float omega_mask,
+                                   float omega_edit, int32_t *new_tokens, float *conf, uint8_t *action,
+                                   uint8_t *block_changed, int32_t *changed_count, float *entropy,
+                                   const int32_t *run_if_nonzero, void *workspace, void *stream) {
+  int32_t chunks;
+  int64_t len;
+  edit_select_plan(rows, vocab, &chunks, &len);
+  EsParams p{};
+  p.logits = static_cast<const uint16_t *>(logits);
+  p.rows = rows;
+  p.vocab = vocab;
+  p.ld = row_stride;
+  p.chunk_len = len;
+  p.chunks = chunks;
+  p.update = 1;
+  p.cur = cur_tokens;
+  p.threshold = omega_edit;
+  p.new_tokens = new_tokens;
+  p.conf = conf;
+  char *ws = static_cast<char *>(workspace);
+  p.pred = reinterpret_cast<int32_t *>(ws);
+  if (chunks > 1) p.partials = reinterpret_cast<EsPartial *>(ws + align_up(static_cast<size_t>(rows) * 4));
+  p.entropy = entropy;
+  p.changed_count = changed_count;
+  p.action = action;
+  p.block_changed = block_changed;
+  p.mask_id = mask_id;
+  p.block_size = block_size;
+  p.omega_mask = omega_mask;
+  p.gate = run_if_nonzero;
+  const bool vec = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && (row_stride % 8 == 0);
+  hipError_t e = launch_threshold_update(p, vec, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "threshold update launch");
+  return MBE_OK;
+}
+
+}  // namespace mbe
 
 extern "C" {
 
@@ -577,59 +723,22 @@ size_t mbe_threshold_update_workspace_size(int64_t rows, int64_t vocab) {
 mbe_status mbe_threshold_update(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
                                 const int32_t *cur_tokens, int32_t mask_id, int32_t block_size, float omega_mask,
                                 float omega_edit, int32_t *new_tokens, float *conf, uint8_t *action,
-                                uint8_t *block_changed, int32_t *changed_count, float *entropy, void *workspace,
-                                size_t workspace_bytes, void *stream) {
-  if (rows < 0 || vocab < 0) return fail(MBE_ERR_BAD_SHAPE, "rows %lld / vocab %lld negative",
-                                         static_cast<long long>(rows), static_cast<long long>(vocab));
-  if (rows > 0 && vocab < 1) return fail(MBE_ERR_BAD_SHAPE, "vocab must be >= 1");
-  if (row_stride < vocab)
-    return fail(MBE_ERR_BAD_SHAPE, "row_stride %lld < vocab %lld", static_cast<long long>(row_stride),
-                static_cast<long long>(vocab));
-  if (vocab > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "vocab beyond int32 indices");
-  if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
-  if (rows % block_size != 0)
-    return fail(MBE_ERR_BAD_SHAPE, "rows %lld is not a multiple of block_size %d", static_cast<long long>(rows),
-                block_size);
-  if (omega_mask != omega_mask || omega_edit != omega_edit) return fail(MBE_ERR_BAD_VALUE, "threshold is NaN");
-  if (rows == 0) return MBE_OK;
-  if (!logits || !cur_tokens || !new_tokens || !conf || !action || !block_changed)
-    return fail(MBE_ERR_NULL_ARG, "logits, cur_tokens, new_tokens, conf, action and block_changed must be non-NULL");
-  int32_t chunks;
-  int64_t len;
-  mbe::edit_select_plan(rows, vocab, &chunks, &len);
-  if (rows * chunks > 0x7fffffffLL) return fail(MBE_ERR_BAD_SHAPE, "too many rows");
-  const size_t need = mbe_threshold_update_workspace_size(rows, vocab);
+                                uint8_t *block_changed, int32_t *changed_count, float *entropy,
+                                const int32_t *run_if_nonzero, void *workspace, size_t workspace_bytes,
+                                void *stream) {
+  size_t need = 0;
+  mbe_status st = mbe::threshold_update_check(logits, rows, vocab, row_stride, cur_tokens, block_size, omega_mask,
+                                              omega_edit, new_tokens, conf, action, block_changed, changed_count,
+                                              run_if_nonzero, &need);
+  if (st != MBE_OK || rows == 0) return st;
   if (!workspace) return fail(MBE_ERR_WORKSPACE, "workspace of %zu bytes required", need);
   if (workspace_bytes < need)
     return fail(MBE_ERR_WORKSPACE, "workspace %zu bytes < required %zu", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return fail(MBE_ERR_WORKSPACE, "workspace must be 256-byte aligned");
-  mbe::EsParams p{};
-  p.logits = static_cast<const uint16_t *>(logits);
-  p.rows = rows;
-  p.vocab = vocab;
-  p.ld = row_stride;
-  p.chunk_len = len;
-  p.chunks = chunks;
-  p.update = 1;
-  p.cur = cur_tokens;
-  p.threshold = omega_edit;
-  p.new_tokens = new_tokens;
-  p.conf = conf;
-  char *ws = static_cast<char *>(workspace);
-  p.pred = reinterpret_cast<int32_t *>(ws);
-  if (chunks > 1) p.partials = reinterpret_cast<mbe::EsPartial *>(ws + align_up(static_cast<size_t>(rows) * 4));
-  p.entropy = entropy;
-  p.changed_count = changed_count;
-  p.action = action;
-  p.block_changed = block_changed;
-  p.mask_id = mask_id;
-  p.block_size = block_size;
-  p.omega_mask = omega_mask;
-  const bool vec = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) && (row_stride % 8 == 0);
-  hipError_t e = mbe::launch_threshold_update(p, vec, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "threshold update launch");
-  return MBE_OK;
+  return mbe::threshold_update_launch(logits, rows, vocab, row_stride, cur_tokens, mask_id, block_size, omega_mask,
+                                      omega_edit, new_tokens, conf, action, block_changed, changed_count, entropy,
+                                      run_if_nonzero, workspace, stream);
 }
 
 mbe_status mbe_tail_entropy_scores(const float *entropy, int64_t num_blocks, int32_t block_size, float rho,
@@ -668,13 +777,14 @@ mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t sc
 mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads, int32_t head_dim,
                         const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *start_pos,
                         const int32_t *lens, int32_t batch, int32_t max_len, int32_t total_tokens, const void *k_new,
-                        const void *v_new, void *stream) {
+                        const void *v_new, const uint8_t *block_flags, int32_t block_size, void *stream) {
   if (head_dim != 64 && head_dim != 128)
     return fail(MBE_ERR_UNSUPPORTED, "head_dim %d: supported are 64 and 128", head_dim);
   if (num_kv_heads < 1 || num_kv_heads > 65535) return fail(MBE_ERR_BAD_SHAPE, "num_kv_heads %d", num_kv_heads);
   if (batch < 0 || batch > 65535) return fail(MBE_ERR_BAD_SHAPE, "batch %d outside [0, 65535]", batch);
   if (max_len < 0 || total_tokens < 0 || num_pages < 0 || max_pages_per_seq < 0)
     return fail(MBE_ERR_BAD_SHAPE, "negative max_len/total_tokens/num_pages/max_pages_per_seq");
+  if (block_flags && block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1 with block flags", block_size);
   if (batch == 0 || max_len == 0 || total_tokens == 0) return MBE_OK;
   if (num_pages < 1 || max_pages_per_seq < 1) return fail(MBE_ERR_BAD_SHAPE, "empty page pool or table");
   if (!k_pages || !v_pages || !page_table || !start_pos || !lens || !k_new || !v_new)
@@ -682,6 +792,13 @@ mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t
   if ((reinterpret_cast<uintptr_t>(k_pages) | reinterpret_cast<uintptr_t>(v_pages) |
        reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new)) % 16 != 0)
     return fail(MBE_ERR_BAD_SHAPE, "pools and k_new/v_new must be 16-byte aligned");
+  const int32_t flag_stride = block_flags ? (max_len + block_size - 1) / block_size : 0;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (debug_checks()) {
+    mbe_status s = debug_check_kv_write(page_table, max_pages_per_seq, num_pages, start_pos, lens, batch, max_len,
+                                        total_tokens, st);
+    if (s != MBE_OK) return s;
+  }
   mbe::KvWriteParams p{};
   p.k_pages = static_cast<uint16_t *>(k_pages);
   p.v_pages = static_cast<uint16_t *>(v_pages);
@@ -697,7 +814,10 @@ mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t
   p.total_tokens = total_tokens;
   p.k_new = static_cast<const uint16_t *>(k_new);
   p.v_new = static_cast<const uint16_t *>(v_new);
-  hipError_t e = mbe::launch_kv_write(p, static_cast<hipStream_t>(stream));
+  p.block_flags = block_flags;
+  p.block_size = block_flags ? block_size : 1;
+  p.flag_stride = flag_stride;
+  hipError_t e = mbe::launch_kv_write(p, st);
   if (e != hipSuccess) return hip_fail(e, "kv write launch");
   return MBE_OK;
 }

@@ -218,6 +218,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // later splits (later splits of short sequences have no work).  Either way
   // the qtiles query tiles of a group, which read the same keys, take
   // consecutive slots of one XCD so that the second finds the keys in its L2.
+  if (p.gate && *p.gate == 0) return;     // gated off: the call does nothing
   const int64_t id = blockIdx.x;
   int64_t grp;
   int qtile;
@@ -286,11 +287,14 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int r = row0 + wrow * kRowsPerWave + qb * 32 + c;
-    valid[qb] = r < M && cu + r / G < p.total_q;
+    valid[qb] = r < M && cu + r / G < p.total_q &&
+                (!p.block_flags || p.block_flags[static_cast<int64_t>(b) * p.flag_stride + (r / G) / p.block_size]);
     const int i = valid[qb] ? r / G : 0;
     const int hq = g * G + (valid[qb] ? r % G : 0);
     qoff[qb] = (static_cast<int64_t>(cu + i) * p.num_q_heads + hq) * D;
   }
+  // with block flags, a workgroup none of whose rows is flagged does nothing
+  if (p.block_flags && !__syncthreads_or(valid[0] || valid[1])) return;
   constexpr int KK = D / 16;
   bf16x8 qreg[2][KK];
 #pragma unroll
@@ -659,6 +663,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
 //   M = max m_s,  O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s   (split order).
 template <int D>
 __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams p) {
+  if (p.gate && *p.gate == 0) return;
   const int b = blockIdx.y;
   const int P = min(max(p.prefix_lens[b], 0), p.max_prefix);
   const int W = p.fixed_window >= 0 ? p.fixed_window : min(max(p.window_lens[b], 0), p.max_window);
@@ -682,6 +687,9 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   const int64_t r = item / D4;              // (window row, query head) within the sequence
   const int d0 = static_cast<int>(item % D4) * 4;
   if (cu + r / p.num_q_heads >= p.total_q) return;
+  if (p.block_flags &&
+      !p.block_flags[static_cast<int64_t>(b) * p.flag_stride + (r / p.num_q_heads) / p.block_size])
+    return;                                 // row of an unflagged block: not written
   const int64_t rowidx = static_cast<int64_t>(cu) * p.num_q_heads + r;
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
   // Every split below nsplit wrote this row (zeros and a -inf reference when

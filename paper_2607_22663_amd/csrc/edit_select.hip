@@ -195,6 +195,7 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
   __shared__ float sh_t[kT / 64];
   __shared__ int32_t sh_i[kT / 64];
   if (p.changed_count && blockIdx.x == 0 && threadIdx.x == 0) *p.changed_count = 0;   // counted per block later
+  if (p.gate && *p.gate == 0) return;     // gated off: the block step keeps every row
 
   const int64_t wg = blockIdx.x;
   const int64_t row = wg / p.chunks;
@@ -364,7 +365,7 @@ __global__ __launch_bounds__(kT) void edit_select_kernel(EsParams p) {
 template <bool ENT>
 __global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (row >= p.rows) return;
+  if (row >= p.rows || (p.gate && *p.gate == 0)) return;
   const int lane = threadIdx.x & 63;
   const EsPartial *pp = p.partials + row * p.chunks;
   float m = -INFINITY, s = 0.f, t = 0.f;
@@ -386,12 +387,23 @@ __global__ __launch_bounds__(256) void edit_select_finalize_kernel(EsParams p) {
 
 // Threshold update, second step: one workgroup per block of block_size rows
 // applies the mask-to-token set, the force-unmask and the token-to-token set
-// to the rows' predictions and confidences.
+// to the rows' predictions and confidences.  Each row's current token is read
+// and its new token written by the same thread, so new_tokens may be
+// cur_tokens itself (an in-place update).
 __global__ __launch_bounds__(256) void threshold_block_kernel(EsParams p) {
   __shared__ unsigned long long sh_best;
   __shared__ int32_t sh_changed;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * p.block_size;
   const int tid = threadIdx.x;
+  if (p.gate && *p.gate == 0) {
+    // gated off: the pass changes nothing (its rows were not reduced)
+    for (int i = tid; i < p.block_size; i += 256) {
+      p.action[r0 + i] = 0;
+      p.new_tokens[r0 + i] = p.cur[r0 + i];
+    }
+    if (tid == 0) p.block_changed[blockIdx.x] = 0;
+    return;
+  }
   if (tid == 0) {
     sh_best = 0;
     sh_changed = 0;
@@ -441,28 +453,6 @@ __global__ __launch_bounds__(256) void threshold_block_kernel(EsParams p) {
 }
 
 }  // namespace
-
-void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len) {
-  // Enough workgroups to cover the 256 CUs twice; a chunk keeps at least 4096
-  // elements, one full iteration of the workgroup.  (Measured on 64 rows of
-  // 131072: 512 workgroups of 4 iterations beat 2048 of one, whose time is
-  // dispatch and one memory round trip.)
-  const int64_t target_wgs = 512;
-  int64_t c = 1;
-  if (rows < target_wgs) {
-    c = (target_wgs + rows - 1) / rows;
-    const int64_t max_c = (vocab + 4095) / 4096;
-    if (c > max_c) c = max_c;
-    if (c > 1024) c = 1024;
-    if (c < 1) c = 1;
-  }
-  int64_t len = (vocab + c - 1) / c;
-  len = (len + 7) / 8 * 8;
-  c = (vocab + len - 1) / len;
-  if (c < 1) c = 1;
-  *chunks = static_cast<int32_t>(c);
-  *chunk_len = len;
-}
 
 template <bool ENT>
 hipError_t launch_rows(const EsParams &p, bool vector_loads, hipStream_t stream) {

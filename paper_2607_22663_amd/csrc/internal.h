@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "mbe.h"
+
 namespace mbe {
 
 // ---------------------------------------------------------------- attention
@@ -40,6 +42,9 @@ struct AttnParams {
   int64_t groups;             // (split, sequence rank, KV head) groups of qtiles work units
   int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
+  const uint8_t *block_flags; // [batch][flag_stride] or null: rows of unflagged window blocks are skipped
+  int32_t flag_stride;
+  const int32_t *gate;        // device int32 or null: the call does nothing when *gate == 0
   // Dispatch order, from the host lengths when given.
   //   kOrderSeqs:  order[rank] is the sequence of that rank (longest first);
   //                groups are dealt round-robin to the XCDs by formula.
@@ -87,6 +92,7 @@ struct EsParams {
   uint8_t *block_changed;   // [rows / block_size]
   int32_t mask_id, block_size;
   float omega_mask;
+  const int32_t *gate;      // threshold update: when *gate == 0 the pass changes nothing
 };
 
 void edit_select_plan(int64_t rows, int64_t vocab, int32_t *chunks, int64_t *chunk_len);
@@ -109,8 +115,27 @@ struct KvWriteParams {
   const int32_t *start_pos, *lens;
   int32_t batch, max_len, total_tokens;
   const uint16_t *k_new, *v_new;   // bf16 [total_tokens][heads][D]
+  const uint8_t *block_flags;      // [batch][flag_stride], or null: write every token
+  int32_t block_size, flag_stride; // token t of a sequence is in block t / block_size
 };
 hipError_t launch_kv_write(const KvWriteParams &p, hipStream_t stream);
+
+// ------------------------------------------------- shared by the C entry points
+// Sets the thread-local error string; returns s.
+mbe_status report(mbe_status s, const char *fmt, ...);
+// Argument checks of the threshold update (all but the workspace); *need
+// receives the workspace bytes the call uses (0 when rows == 0).
+mbe_status threshold_update_check(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                  const int32_t *cur_tokens, int32_t block_size, float omega_mask, float omega_edit,
+                                  const int32_t *new_tokens, const float *conf, const uint8_t *action,
+                                  const uint8_t *block_changed, const int32_t *changed_count,
+                                  const int32_t *run_if_nonzero, size_t *need);
+// Launches a checked threshold update on a workspace of at least *need bytes.
+mbe_status threshold_update_launch(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                   const int32_t *cur_tokens, int32_t mask_id, int32_t block_size, float omega_mask,
+                                   float omega_edit, int32_t *new_tokens, float *conf, uint8_t *action,
+                                   uint8_t *block_changed, int32_t *changed_count, float *entropy,
+                                   const int32_t *run_if_nonzero, void *workspace, void *stream);
 
 
 }  // namespace mbe

@@ -4,12 +4,17 @@
 // leaves the cache untouched; afterwards the changed blocks are recomputed
 // under standard attention and their K/V written back.  This kernel is that
 // write: token t of sequence b goes to absolute position start_b + t, i.e.
-// slot (position % 16) of page page_table[b][position / 16].
+// slot (position % 16) of page page_table[b][position / 16].  With block
+// flags only the tokens of flagged blocks (block t / B of the write) are
+// written: the blocks the refresh recomputed.
 //
-// One workgroup per (sequence, page touched, KV head).  K rows are copied as
-// 16-byte chunks.  V is token-minor in the pool ([D][16] per page and head):
-// the workgroup stages its tokens' V rows in LDS, then writes each dim's run
-// of slots, 16 bytes at a time where all 8 slots of a half-row are in range.
+// One workgroup per (sequence, page touched, KV head).  The workgroup first
+// decides which of the page's 16 slots it writes (in range, a row of the
+// input, a flagged block), then copies K rows as 16-byte chunks.  V is
+// token-minor in the pool ([D][16] per page and head): the workgroup stages
+// its tokens' V rows in LDS, then writes each dim's run of slots, 16 bytes at
+// a time where all 8 slots of a half-row are written.  A table slot past the
+// row or a page id outside the pool writes nothing.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -29,41 +34,47 @@ __global__ __launch_bounds__(256) void kv_write_kernel(KvWriteParams p) {
   const int page_slot = start / kPageSize + static_cast<int>(blockIdx.x);   // page index within the row
   const int p0 = max(start, page_slot * kPageSize);                          // positions [p0, p1) on this page
   const int p1 = min(start + len, (page_slot + 1) * kPageSize);
-  if (p0 >= p1) return;
+  if (p0 >= p1 || page_slot >= p.max_pages) return;
+  const int32_t pid = p.page_table[static_cast<int64_t>(b) * p.max_pages + page_slot];
+  if (pid < 0 || pid >= p.num_pages) return;
   // first row of sequence b: the lengths before it, summed across the lanes
   // of the wave (independent loads, then a butterfly)
   int64_t row0 = 0;
   for (int j = threadIdx.x & 63; j < b; j += 64) row0 += min(max(p.lens[j], 0), p.max_len);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) row0 += __shfl_xor(row0, o);
-  const int slot_row = min(page_slot, p.max_pages - 1);
-  const int64_t page = min(max(p.page_table[static_cast<int64_t>(b) * p.max_pages + slot_row], 0), p.num_pages - 1);
-  const int64_t page_base = (page * p.num_kv_heads + g) * static_cast<int64_t>(kPageSize) * D;   // elements
+  // slots of this page that are written: bit s for slot s (same in every lane)
+  uint32_t wmask = 0;
+  for (int pos = p0; pos < p1; ++pos) {
+    const int t = pos - start;
+    const bool in_rows = row0 + t < p.total_tokens;
+    const bool flagged = !p.block_flags || p.block_flags[static_cast<int64_t>(b) * p.flag_stride + t / p.block_size];
+    if (in_rows && flagged) wmask |= 1u << (pos % kPageSize);
+  }
+  if (wmask == 0) return;
+  const int64_t page_base = (static_cast<int64_t>(pid) * p.num_kv_heads + g) * kPageSize * D;   // elements
   const int chunks = D / 8;
   const int n = p1 - p0;
-  // K: [slot][D], a 16-byte chunk per thread
+  // K: [slot][D], a 16-byte chunk per thread; V rows staged in LDS as [slot][D]
   for (int i = threadIdx.x; i < n * chunks; i += 256) {
     const int tok = i / chunks, c = i % chunks;
+    const int slot = (p0 + tok) % kPageSize;
+    if (!((wmask >> slot) & 1u)) continue;
     const int64_t row = row0 + (p0 - start) + tok;
-    if (row >= p.total_tokens) continue;
-    const uint4 w = *reinterpret_cast<const uint4 *>(p.k_new + (row * p.num_kv_heads + g) * D + c * 8);
-    *reinterpret_cast<uint4 *>(p.k_pages + page_base + ((p0 + tok) % kPageSize) * D + c * 8) = w;
-  }
-  // V: stage [slot][D] in LDS, then write [D][slot]
-  for (int i = threadIdx.x; i < n * chunks; i += 256) {
-    const int tok = i / chunks, c = i % chunks;
-    const int64_t row = row0 + (p0 - start) + tok;
-    uint4 w = make_uint4(0, 0, 0, 0);
-    if (row < p.total_tokens) w = *reinterpret_cast<const uint4 *>(p.v_new + (row * p.num_kv_heads + g) * D + c * 8);
-    *reinterpret_cast<uint4 *>(vs + ((p0 + tok) % kPageSize) * D + c * 8) = w;
+    const uint4 wk = *reinterpret_cast<const uint4 *>(p.k_new + (row * p.num_kv_heads + g) * D + c * 8);
+    *reinterpret_cast<uint4 *>(p.k_pages + page_base + slot * D + c * 8) = wk;
+    *reinterpret_cast<uint4 *>(vs + slot * D + c * 8) =
+        *reinterpret_cast<const uint4 *>(p.v_new + (row * p.num_kv_heads + g) * D + c * 8);
   }
   __syncthreads();
-  const int s0 = p0 % kPageSize, s1 = s0 + n;       // slots [s0, s1) on this page
-  for (int i = threadIdx.x; i < D * 2; i += 256) {   // (dim, half of 8 slots)
+  // V: [D][slot], per (dim, half of 8 slots)
+  for (int i = threadIdx.x; i < D * 2; i += 256) {
     const int d = i >> 1, h = i & 1;
-    const int a = h * 8, e = a + 8;
+    const int a = h * 8;
+    const uint32_t half = (wmask >> a) & 0xFFu;
+    if (half == 0) continue;
     uint16_t *dst = p.v_pages + page_base + static_cast<int64_t>(d) * kPageSize + a;
-    if (s0 <= a && e <= s1) {
+    if (half == 0xFFu) {
       uint4 w;
       uint32_t *u = reinterpret_cast<uint32_t *>(&w);
 #pragma unroll
@@ -71,7 +82,8 @@ __global__ __launch_bounds__(256) void kv_write_kernel(KvWriteParams p) {
         u[k] = static_cast<uint32_t>(vs[(a + 2 * k) * D + d]) | (static_cast<uint32_t>(vs[(a + 2 * k + 1) * D + d]) << 16);
       *reinterpret_cast<uint4 *>(dst) = w;
     } else {
-      for (int s = max(a, s0); s < min(e, s1); ++s) dst[s - a] = vs[s * D + d];
+      for (int s = 0; s < 8; ++s)
+        if ((half >> s) & 1u) dst[s] = vs[(a + s) * D + d];
     }
   }
 }

@@ -122,3 +122,99 @@ class EditPassGraphs:
         if g is None:
             raise KeyError(f"no graph captured for shape {key}")
         g.replay()
+
+
+class PassLoopGraph:
+    """At most N_MBE editing passes captured as one graph, stopping early on
+    the device (paper, Sec. "Training-Free MBE Decoding": at most N_MBE
+    cross-block passes, stopping when no token changes).
+
+    Pass n runs window attention over the paged cache and the full threshold
+    update, in place on one token buffer.  Every pass after the first is gated
+    on the previous pass's changed count (`run_if_nonzero`): once a pass
+    changes nothing, the later passes' kernels exit at once, so a converged
+    loop costs about a launch per remaining pass and needs no host read.
+
+    The per-pass queries and logits are static inputs (`q[n]`, `logits[n]`):
+    in a full decoder they come from the model forward on the current tokens,
+    which lies outside this library.  Outputs per pass: `out[n]` (attention),
+    `conf[n]`, `action[n]`, `block_changed[n]`, `counts[n]`; a gated-off pass
+    leaves `out[n]` and `conf[n]` as they were and reports no change.
+    """
+
+    def __init__(self, *, k_pages, v_pages, batch, window, block_size, num_q_heads, max_pages_per_seq,
+                 max_prefix_len, vocab, mask_id, n_passes=5, omega_mask=0.5, omega_edit=0.0):
+        dev = k_pages.device
+        D = k_pages.shape[3]
+        self.dev = dev
+        self.k_pages, self.v_pages = k_pages, v_pages
+        self.batch, self.window, self.block_size = int(batch), int(window), int(block_size)
+        if self.window % self.block_size or self.window < 1 or self.batch < 1:
+            raise ValueError("window must be a positive multiple of block_size")
+        self.n_passes = int(n_passes)
+        self.max_prefix_len = int(max_prefix_len)
+        self.vocab, self.mask_id = int(vocab), int(mask_id)
+        self.omega_mask, self.omega_edit = float(omega_mask), float(omega_edit)
+        T = self.batch * self.window
+        n = self.n_passes
+        self.q = torch.zeros(n, T, num_q_heads, D, dtype=torch.bfloat16, device=dev)
+        self.out = torch.zeros_like(self.q)
+        self.logits = torch.zeros(n, T, self.vocab, dtype=torch.bfloat16, device=dev)
+        self.page_table = torch.zeros(self.batch, max_pages_per_seq, dtype=torch.int32, device=dev)
+        self.prefix_lens = torch.zeros(self.batch, dtype=torch.int32, device=dev)
+        self.window_lens = torch.full((self.batch,), self.window, dtype=torch.int32, device=dev)
+        self.tokens = torch.zeros(T, dtype=torch.int32, device=dev)
+        self.conf = torch.zeros(n, T, dtype=torch.float32, device=dev)
+        self.action = torch.zeros(n, T, dtype=torch.uint8, device=dev)
+        self.block_changed = torch.zeros(n, T // self.block_size, dtype=torch.uint8, device=dev)
+        self.counts = torch.zeros(n, dtype=torch.int32, device=dev)
+        a = workspace_bytes_window_attention(self.q[0], k_pages, self.page_table, self.batch, self.block_size,
+                                             max_prefix_len=self.max_prefix_len, max_window_len=self.window)
+        u = workspace_bytes_threshold_update(T, self.vocab)
+        self._ws_attn = torch.empty(max(a, 1), dtype=torch.uint8, device=dev)
+        self._ws_upd = torch.empty(max(u, 1), dtype=torch.uint8, device=dev)
+        self.graph = None
+
+    def _pass(self, i):
+        gate = None if i == 0 else self.counts[i - 1:i]
+        window_attention(self.q[i], self.k_pages, self.v_pages, self.page_table, self.prefix_lens, self.window_lens,
+                         self.block_size, out=self.out[i], max_prefix_len=self.max_prefix_len,
+                         max_window_len=self.window, workspace=self._ws_attn, run_if_nonzero=gate)
+        out = {"new_tokens": self.tokens, "conf": self.conf[i], "action": self.action[i],
+               "block_changed": self.block_changed[i], "changed_count": self.counts[i:i + 1]}
+        threshold_update(self.logits[i], self.tokens, self.mask_id, self.block_size, self.omega_mask,
+                         self.omega_edit, out=out, workspace=self._ws_upd, run_if_nonzero=gate)
+
+    def run_eager(self, i):
+        """Pass i alone, ungated (for host-driven loops and checks)."""
+        window_attention(self.q[i], self.k_pages, self.v_pages, self.page_table, self.prefix_lens, self.window_lens,
+                         self.block_size, out=self.out[i], max_prefix_len=self.max_prefix_len,
+                         max_window_len=self.window, workspace=self._ws_attn)
+        out = {"new_tokens": self.tokens, "conf": self.conf[i], "action": self.action[i],
+               "block_changed": self.block_changed[i], "changed_count": self.counts[i:i + 1]}
+        threshold_update(self.logits[i], self.tokens, self.mask_id, self.block_size, self.omega_mask,
+                         self.omega_edit, out=out, workspace=self._ws_upd)
+
+    def capture(self):
+        """Capture the N_MBE gated passes (once; the static inputs may be
+        refilled between replays).  Runs the passes once eagerly first (the
+        warm-up), which changes `tokens`: set the tokens after capturing."""
+        if self.graph is not None:
+            return
+        side = torch.cuda.Stream(device=self.dev)
+        side.wait_stream(torch.cuda.current_stream(self.dev))
+        with torch.cuda.stream(side):
+            for i in range(self.n_passes):
+                self._pass(i)
+        torch.cuda.current_stream(self.dev).wait_stream(side)
+        torch.cuda.synchronize(self.dev)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(self.n_passes):
+                self._pass(i)
+        self.graph = g
+
+    def replay(self):
+        if self.graph is None:
+            raise RuntimeError("capture() first")
+        self.graph.replay()

@@ -187,17 +187,18 @@ def _vp(x):
     (dict(ws=None), 4, "workspace"),
     (dict(wsb=16), 4, "workspace"),
     (dict(ws=272), 4, "aligned"),
+    (dict(count=64, gate=64), 6, "run_if_nonzero"),
 ])
 def test_threshold_update_validation(lib, args, status, text):
     a = dict(logits=16, rows=64, vocab=128, row_stride=128, cur=16, mask_id=127, block_size=32, omega_mask=0.5,
-             omega_edit=0.0, new=16, conf=16, action=16, block_changed=16, count=None, entropy=None, ws=256,
-             wsb=1 << 20)
+             omega_edit=0.0, new=16, conf=16, action=16, block_changed=16, count=None, entropy=None, gate=None,
+             ws=256, wsb=1 << 20)
     a.update(args)
     st = lib.mbe_threshold_update(_vp(a["logits"]), a["rows"], a["vocab"], a["row_stride"], _vp(a["cur"]),
                                   a["mask_id"], a["block_size"], ctypes.c_float(a["omega_mask"]),
                                   ctypes.c_float(a["omega_edit"]), _vp(a["new"]), _vp(a["conf"]), _vp(a["action"]),
-                                  _vp(a["block_changed"]), _vp(a["count"]), _vp(a["entropy"]), _vp(a["ws"]),
-                                  a["wsb"], None)
+                                  _vp(a["block_changed"]), _vp(a["count"]), _vp(a["entropy"]), _vp(a["gate"]),
+                                  _vp(a["ws"]), a["wsb"], None)
     assert st == status and text in lib.mbe_last_error().decode(), lib.mbe_last_error()
 
 
@@ -208,7 +209,7 @@ def test_threshold_update_workspace_and_empty(lib):
     assert n >= 8192 * 4 and n % 256 == 0
     assert lib.mbe_threshold_update_workspace_size(64, 131072) > lib.mbe_edit_select_workspace_size(64, 131072)
     assert lib.mbe_threshold_update(None, 0, 128, 128, None, 0, 32, ctypes.c_float(0.5), ctypes.c_float(0.0),
-                                    None, None, None, None, None, None, None, 0, None) == 0
+                                    None, None, None, None, None, None, None, None, 0, None) == 0
 
 
 @pytest.mark.parametrize("args,status,text", [
@@ -248,14 +249,15 @@ def test_select_start_validation(lib, args, status, text):
     (dict(k_new=None), 1, "non-NULL"),
     (dict(v_pages=24), 2, "aligned"),
     (dict(num_pages=0), 2, "empty"),
+    (dict(flags=16, block_size=0), 2, "block_size"),
 ])
 def test_kv_write_validation(lib, args, status, text):
     a = dict(k_pages=16, v_pages=32, num_pages=10, heads=4, head_dim=128, pt=16, max_pages=8, start=16, lens=16,
-             batch=2, max_len=64, total=96, k_new=16, v_new=16)
+             batch=2, max_len=64, total=96, k_new=16, v_new=16, flags=None, block_size=0)
     a.update(args)
     st = lib.mbe_kv_write(_vp(a["k_pages"]), _vp(a["v_pages"]), a["num_pages"], a["heads"], a["head_dim"],
                           _vp(a["pt"]), a["max_pages"], _vp(a["start"]), _vp(a["lens"]), a["batch"], a["max_len"],
-                          a["total"], _vp(a["k_new"]), _vp(a["v_new"]), None)
+                          a["total"], _vp(a["k_new"]), _vp(a["v_new"]), _vp(a["flags"]), a["block_size"], None)
     assert st == status and text in lib.mbe_last_error().decode()
 
 

@@ -271,34 +271,57 @@ def test_deterministic(gpu):
     assert torch.equal(a, b)
 
 
-# ---------------------------------------------------------------- full sizes, sampled
-def _sampled_parity(gpu, case, seqs, what, **kw):
-    out = run_case(gpu, case, "bidir", **kw)
+# ---------------------------------------------------------------- benchmark sizes, every sequence
+def _per_sequence_parity(gpu, case, seqs, what, mode="bidir", **kw):
+    """One call over the whole batch at its benchmark shape (the launch the
+    bench times); the oracle then runs sequence by sequence on the rows of
+    `seqs` (every sequence unless a subset is given)."""
+    out = run_case(gpu, case, mode, **kw)
+    m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
+    worst = (0.0, 0.0)
     for b in seqs:
         q, pt, P, W, rows = seq_slice(case, b)
-        ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size)
-        err = assert_attn_close(out[rows], ref, f"{what} seq {b}")
-        say(f"  {what} seq {b} P={int(P[0])}: max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
+        ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size, m)
+        err = assert_attn_close(out[rows], ref, f"{what} {mode} seq {b}")
+        worst = (max(worst[0], err[0]), max(worst[1], err[1]))
+        say(f"  {what} {mode} seq {b} P={int(P[0])}: max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
+    say(f"  {what} {mode}: {len(seqs)} sequences, worst max_abs {worst[0]:.2e} rel_rms {worst[1]:.2e}")
 
 
-def test_batch32_sampled(gpu):
+def test_batch32_every_sequence(gpu):
     case = synth.workload_attention("batch32_p512to8192_k2")
-    P = case.prefix_lens.numpy()
-    seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 7})
-    _sampled_parity(gpu, case, seqs, "batch32")
+    _per_sequence_parity(gpu, case, range(case.batch), "batch32")
 
 
 @pytest.mark.parametrize("k", synth.SPAN_SWEEP_K)
-def test_span_sweep_sampled(gpu, k):
+def test_span_sweep_every_sequence(gpu, k):
     case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=k)
-    _sampled_parity(gpu, case, [0, 5], f"span k={k}")
+    _per_sequence_parity(gpu, case, range(case.batch), f"span k={k}")
 
 
-def test_long_context_sampled(gpu):
+def test_long_context_every_sequence(gpu):
+    """All 64 sequences of the long-context workload (prefixes 4K-32K, 4-block
+    windows) against the oracle."""
+    case = synth.workload_attention("long_context_b64_p4096to32768_k4")
+    _per_sequence_parity(gpu, case, range(case.batch), "long_context")
+
+
+def test_long_context_block_causal_sampled(gpu):
+    """Block-causal (the refresh scope) at the long-context shape, 4 blocks of
+    32 with prefixes up to 32K: the longest, the shortest and two other
+    sequences against the oracle (the launch covers all 64)."""
     case = synth.workload_attention("long_context_b64_p4096to32768_k4")
     P = case.prefix_lens.numpy()
-    seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 31})
-    _sampled_parity(gpu, case, seqs, "long_context")
+    seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 9, 40})
+    _per_sequence_parity(gpu, case, seqs, "long_context", mode="block_causal")
+
+
+def test_span_sweep_block_causal_k4_split(gpu):
+    """Block-causal with 4 blocks over a 16K prefix and forced 1024-key
+    splits (the split-KV merge under the block-causal mask), every sequence."""
+    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=4)
+    _per_sequence_parity(gpu, case, range(case.batch), "span k=4 split 1024", mode="block_causal",
+                         kv_split_tokens=1024)
 
 
 def test_debug_check_rejects_bad_device_values(gpu, monkeypatch):

@@ -55,24 +55,19 @@ def test_batch32_full_parity(gpu):
     check(res, ref, case.threshold, "batch32")
 
 
-def test_long_context_sampled(gpu):
+def test_long_context_every_row(gpu):
+    """8192 x 131072 at the benchmark size: every row against the oracle."""
     case = synth.workload_edit("long_context_b64_p4096to32768_k4", cur_hit_fraction=0.25)
     res = run(gpu, case.logits, case.cur_tokens, case.threshold)
-    rng = np.random.default_rng(0)
-    rows = np.sort(np.concatenate([rng.choice(case.logits.shape[0], 384, replace=False),
-                                   case.planted_rows[:64]]))
-    rows = np.unique(rows)
-    ref = oracle.edit_select(case.logits[torch.from_numpy(rows)], case.cur_tokens[torch.from_numpy(rows)],
-                             case.threshold)
-    check(res, ref, case.threshold, "long_context sampled", rows=rows)
-    # every row: the selected token attains the row maximum and no earlier column does
-    L = case.logits.float()
-    mx = L.max(dim=1).values
-    first = (L == mx[:, None]).int().argmax(dim=1).numpy()
-    cur = case.cur_tokens.numpy()
-    n, _, ch = res
-    assert np.array_equal(np.where(ch == 1, n, first), first)
-    assert np.all((ch == 0) | (n != cur))
+    R = case.logits.shape[0]
+    refs = []
+    for r0 in range(0, R, 1024):
+        sl = slice(r0, r0 + 1024)
+        refs.append(oracle.edit_select(case.logits[sl], case.cur_tokens[sl], case.threshold))
+        say(f"  oracle rows {r0}..{r0 + 1023}")
+    ref = tuple(np.concatenate([x[i] for x in refs]) for i in range(3))
+    rel = check(res, ref, case.threshold, "long_context")
+    say(f"  rows {R} changed {int(res[2].sum())} conf rel err {rel:.2e}")
 
 
 def test_special_rows_pin_ge_and_ties(gpu):

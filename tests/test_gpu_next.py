@@ -52,13 +52,20 @@ def update_case(name, seed, *, block=32, mask_frac=0.4, rows=None, ties=True):
 
 
 def safe(L64_conf, cur, mask_id, block, om, oe):
+    """Checks that no confidence lies within MARGIN of a threshold, and
+    returns the blocks whose force-unmask choice fp32 cannot decide: no
+    masked row clears omega_mask and the two highest masked confidences
+    differ by less than MARGIN relative (without being equal).  There any
+    masked row within MARGIN of the maximum is a correct choice."""
     c = np.asarray(L64_conf)
     assert np.all(np.abs(c - om) >= MARGIN) and np.all(np.abs(c - oe) >= MARGIN), "confidence too close to a threshold"
     curn = cur.numpy()
+    ambiguous = []
     for k in range(len(c) // block):
         cm = np.sort(c[k * block:(k + 1) * block][curn[k * block:(k + 1) * block] == mask_id])
-        gaps = np.diff(cm)
-        assert np.all((gaps == 0) | (gaps >= MARGIN * cm[1:])), "masked confidences too close to each other"
+        if len(cm) >= 2 and cm[-1] <= om and 0 < cm[-1] - cm[-2] < MARGIN * cm[-1]:
+            ambiguous.append(k)
+    return ambiguous
 
 
 def run_update(mbe, L, cur, mask_id, block, om, oe, entropy=True):
@@ -67,11 +74,26 @@ def run_update(mbe, L, cur, mask_id, block, om, oe, entropy=True):
     return {k: v.cpu().numpy() for k, v in out.items()}
 
 
-def compare_update(got, ref, what, rows=None, block_ids=None):
+def compare_update(got, ref, what, rows=None, block_ids=None, ambiguous=(), cur=None, mask_id=None, block=None):
+    """Bit-exact actions and tokens, except in `ambiguous` blocks (see safe),
+    where the GPU's force-unmask row only has to be a valid choice."""
     sl = slice(None) if rows is None else rows
+    skip = np.zeros(len(ref["action"]), dtype=bool)
+    for k in ambiguous:
+        r = np.arange(k * block, (k + 1) * block)
+        ga, ra = got["action"][sl][r], ref["action"][r]
+        forced = r[ga == 2]
+        assert len(forced) == 1, f"{what}: block {k} has {len(forced)} force-unmasked rows"
+        cm = ref["conf"][r][cur[r] == mask_id]
+        f = forced[0]
+        assert cur[f] == mask_id and ref["conf"][f] >= cm.max() * (1 - MARGIN), f"{what}: invalid force-unmask row {f}"
+        others = (ra != 2) & (ga != 2)
+        assert np.array_equal(ga[others], ra[others]), f"{what}: block {k} differs beyond the force-unmask choice"
+        assert np.array_equal(got["new_tokens"][sl][r][others], ref["new_tokens"][r][others])
+        skip[r] = True
     for key in ("new_tokens", "action"):
         g = got[key][sl]
-        bad = np.nonzero(g != ref[key])[0]
+        bad = np.nonzero((g != ref[key]) & ~skip)[0]
         assert bad.size == 0, f"{what}: {key} differs at rows {bad[:8]}: gpu {g[bad[:5]]} ref {ref[key][bad[:5]]}"
     bc = got["block_changed"] if block_ids is None else got["block_changed"][block_ids]
     assert np.array_equal(bc, ref["block_changed"]), f"{what}: block_changed differs"
@@ -91,9 +113,9 @@ def test_update_full_parity(gpu, name, block, oe):
     """Whole workloads; 64 rows x 131072 also runs the chunked path."""
     L, cur, mid = update_case(name, 1, block=block)
     ref = oracle.threshold_update(L, cur, mid, block, 0.5, oe, with_entropy=True)
-    safe(ref["conf"], cur, mid, block, 0.5, oe)
+    amb = safe(ref["conf"], cur, mid, block, 0.5, oe)
     got = run_update(gpu, L, cur, mid, block, 0.5, oe)
-    rel = compare_update(got, ref, name)
+    rel = compare_update(got, ref, name, ambiguous=amb, cur=cur.numpy(), mask_id=mid, block=block)
     assert int(got["changed_count"][0]) == ref["changed_count"]
     say(f"  rows {L.shape[0]} actions {np.bincount(got['action'], minlength=4)} conf rel {rel:.1e}")
 
@@ -125,24 +147,25 @@ def test_update_entropy_with_neg_inf_logits(gpu):
         assert np.array_equal(got[key][16:], plain[key][16:]), key
 
 
-def test_update_long_context_sampled(gpu):
-    """8192 x 131072 at the benchmark size: 24 blocks against the oracle, the
-    counts and flags of all 256 blocks by their definitions."""
+def test_update_long_context_every_block(gpu):
+    """8192 x 131072 at the benchmark size: all 256 blocks against the oracle
+    (run 32 blocks at a time; blocks are independent)."""
     L, cur, mid = update_case("long_context_b64_p4096to32768_k4", 2)
     B = 32
     got = run_update(gpu, L, cur, mid, B, 0.5, 0.0)
-    blocks = np.random.default_rng(3).choice(L.shape[0] // B, 24, replace=False)
-    rows = np.concatenate([np.arange(k * B, (k + 1) * B) for k in blocks])
-    ref = oracle.threshold_update(L[torch.from_numpy(rows)], cur[torch.from_numpy(rows)], mid, B, 0.5, 0.0,
-                                  with_entropy=True)
-    safe(ref["conf"], cur[torch.from_numpy(rows)], mid, B, 0.5, 0.0)
-    compare_update(got, ref, "long-context blocks", rows=rows, block_ids=blocks)
-    act = got["action"].reshape(-1, B)
-    assert int(got["changed_count"][0]) == int(np.count_nonzero(act))
-    assert np.array_equal(got["block_changed"], np.any(act != 0, axis=1).astype(np.uint8))
-    masked = cur.numpy().reshape(-1, B) == mid
-    assert np.all(np.any(act != 0, axis=1) | ~np.any(masked, axis=1))     # every block with masks unmasks one
-    assert np.all(np.sum(act == 2, axis=1) <= 1)
+    parts = []
+    for r0 in range(0, L.shape[0], 32 * B):
+        sl = slice(r0, r0 + 32 * B)
+        parts.append(oracle.threshold_update(L[sl], cur[sl], mid, B, 0.5, 0.0, with_entropy=True))
+        say(f"  oracle rows {r0}..{r0 + 32 * B - 1}")
+    ref = {k: np.concatenate([p[k] for p in parts]) for k in ("new_tokens", "conf", "action", "block_changed",
+                                                               "entropy")}
+    ref["changed_count"] = sum(p["changed_count"] for p in parts)
+    amb = safe(ref["conf"], cur, mid, B, 0.5, 0.0)
+    rel = compare_update(got, ref, "long-context, every block", ambiguous=amb, cur=cur.numpy(), mask_id=mid, block=B)
+    say(f"  blocks whose force-unmask fp32 cannot decide: {amb}")
+    assert int(got["changed_count"][0]) == ref["changed_count"]
+    say(f"  blocks {L.shape[0] // B} actions {np.bincount(got['action'], minlength=4)} conf rel {rel:.1e}")
 
 
 def test_update_exact_cases(gpu):

@@ -1,0 +1,354 @@
+"""GPU tests of the targeted refresh (block flags) and of the device-side
+early exit of the editing-pass loop (run_if_nonzero), against the oracle.
+
+Paper, Sec. "Infrastructure Optimization", cache control: after an editing
+pass only the changed blocks are recomputed under standard (block-causal)
+attention and their K/V written back.  Sec. "Training-Free MBE Decoding":
+at most N_MBE cross-block passes, stopping when no token changes.
+
+Bars: attention within max-abs 2e-2 / relative RMS 1e-2 of the fp64 oracle;
+flags, counts, tokens, actions and written pools bit-exact; rows and pools a
+call must not touch keep their sentinel bytes."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import assert_attn_close, say
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+SENTINEL = 7.0        # bf16-exact value that no attention output takes here
+
+
+@pytest.fixture(autouse=True)
+def _name(request):
+    say(f"\n[gpu] {request.node.nodeid}")
+
+
+def _attn_case(seed, P, k=4, B=32, Hq=16, Hkv=4, D=128):
+    spec = synth.AttnSpec(len(P), B, k, ("fixed", 0), Hq, Hkv, D)
+    return synth.make_attention_case(spec, seed, prefix_lens=P, tail_fill=float("nan"))
+
+
+def _attn(gpu, c, case, mode, out=None, **kw):
+    o = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens,
+                             case.block_size, mask_mode=mode, out=out, **kw)
+    torch.cuda.synchronize()
+    return o
+
+
+def _oracle(case, mode, k_pages=None, v_pages=None):
+    m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
+    return oracle.window_attention(case.q, case.k_pages if k_pages is None else k_pages,
+                                   case.v_pages if v_pages is None else v_pages, case.page_table,
+                                   case.prefix_lens, case.window_lens, case.block_size, m)
+
+
+def _row_flags(flags, case):
+    """Per q row: the flag of its window block."""
+    W = case.window_lens.numpy()
+    rows = []
+    for b in range(case.batch):
+        for i in range(int(W[b])):
+            rows.append(bool(flags[b, i // case.block_size]))
+    return np.array(rows, dtype=bool)
+
+
+# ------------------------------------------------------------------ gates
+@pytest.mark.parametrize("split", [0, 256])
+def test_attention_gate(gpu, split):
+    """run_if_nonzero = 0: nothing is written (the merge kernel of a split
+    call included); any other value: the normal result."""
+    case = _attn_case(11, [700, 1500])
+    c = case.to(DEV)
+    zero = torch.zeros(1, dtype=torch.int32, device=DEV)
+    five = torch.full((1,), 5, dtype=torch.int32, device=DEV)
+    for mode in ("bidir", "block_causal"):
+        out = torch.full_like(c.q, SENTINEL)
+        _attn(gpu, c, case, mode, out=out, run_if_nonzero=zero, kv_split_tokens=split)
+        assert torch.all(out == SENTINEL), f"{mode}: gated call wrote its output"
+        _attn(gpu, c, case, mode, out=out, run_if_nonzero=five, kv_split_tokens=split)
+        assert_attn_close(out.cpu(), _oracle(case, mode), f"gate 5 {mode} split {split}")
+
+
+def test_update_gate_and_in_place(gpu):
+    """run_if_nonzero = 0: every row kept, new = cur, no block flagged, count 0,
+    conf and entropy untouched.  In place (new_tokens is cur_tokens): the same
+    as a separate output."""
+    case = synth.workload_edit("single_p2048_k2_gqa16x4_d128", cur_hit_fraction=0.1)
+    L, cur = case.logits.to(DEV), case.cur_tokens.to(DEV)
+    R, B = L.shape[0], 32
+    ref = gpu.threshold_update(L, cur, L.shape[1] - 1, B, 0.5, 0.3, with_entropy=True)
+    torch.cuda.synchronize()
+    assert int(ref["changed_count"].item()) > 0
+    out = {"new_tokens": torch.full((R,), -3, dtype=torch.int32, device=DEV),
+           "conf": torch.full((R,), -1.0, device=DEV), "action": torch.full((R,), 9, dtype=torch.uint8, device=DEV),
+           "block_changed": torch.full((R // B,), 9, dtype=torch.uint8, device=DEV),
+           "changed_count": torch.full((1,), 77, dtype=torch.int32, device=DEV),
+           "entropy": torch.full((R,), -1.0, device=DEV)}
+    zero = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gpu.threshold_update(L, cur, L.shape[1] - 1, B, 0.5, 0.3, out=out, run_if_nonzero=zero)
+    torch.cuda.synchronize()
+    assert torch.equal(out["new_tokens"], cur) and torch.all(out["action"] == 0)
+    assert torch.all(out["block_changed"] == 0) and int(out["changed_count"].item()) == 0
+    assert torch.all(out["conf"] == -1.0) and torch.all(out["entropy"] == -1.0)
+    one = torch.ones(1, dtype=torch.int32, device=DEV)
+    gpu.threshold_update(L, cur, L.shape[1] - 1, B, 0.5, 0.3, out=out, run_if_nonzero=one)
+    torch.cuda.synchronize()
+    for k in ref:
+        assert torch.equal(out[k], ref[k]), k
+    tok = cur.clone()
+    inplace = dict(out, new_tokens=tok)
+    gpu.threshold_update(L, tok, L.shape[1] - 1, B, 0.5, 0.3, out=inplace)
+    torch.cuda.synchronize()
+    assert torch.equal(tok, ref["new_tokens"])
+
+
+# ------------------------------------------------------------------ block flags
+@pytest.mark.parametrize("split", [0, 512])
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_attention_block_flags(gpu, mode, split):
+    """Only rows of flagged window blocks are computed and written; the
+    others keep the sentinel.  Workgroups with no flagged row, with some, and
+    the split-KV merge (split 512)."""
+    case = _attn_case(12, [300, 2100, 64, 1000])
+    c = case.to(DEV)
+    flags = np.array([[0, 1, 0, 0], [1, 1, 1, 1], [0, 0, 0, 0], [0, 0, 1, 1]], dtype=np.uint8)
+    out = torch.full_like(c.q, SENTINEL)
+    _attn(gpu, c, case, mode, out=out, block_flags=torch.from_numpy(flags).to(DEV), kv_split_tokens=split)
+    got = out.cpu()
+    rf = torch.from_numpy(_row_flags(flags, case))
+    assert torch.all(got[~rf] == SENTINEL), "an unflagged row was written"
+    ref = _oracle(case, mode)
+    assert_attn_close(got[rf], ref[rf.numpy()], f"flagged rows {mode} split {split}")
+
+
+def test_block_diffusion_flags(gpu):
+    spec = synth.AttnSpec(3, 32, 1, ("fixed", 0), 16, 4, 128)
+    case = synth.make_attention_case(spec, 13, prefix_lens=[500, 64, 1800])
+    c = case.to(DEV)
+    flags = torch.tensor([[1], [0], [1]], dtype=torch.uint8, device=DEV)
+    out = torch.full_like(c.q, SENTINEL)
+    gpu.block_diffusion_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, 32, out=out,
+                                  block_flags=flags)
+    torch.cuda.synchronize()
+    got = out.cpu()
+    assert torch.all(got[32:64] == SENTINEL)
+    ref = oracle.block_diffusion_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens, 32)
+    keep = np.r_[0:32, 64:96]
+    assert_attn_close(got[keep], ref[keep], "block diffusion with flags")
+
+
+def _kv_setup(seed, D=128, Hkv=4):
+    rng = np.random.default_rng(seed)
+    batch, npages, maxp = 4, 120, 24
+    K = torch.from_numpy(rng.normal(size=(npages, Hkv, 16, D)).astype(np.float32)).to(torch.bfloat16)
+    V = torch.from_numpy(rng.normal(size=(npages, Hkv, D, 16)).astype(np.float32)).to(torch.bfloat16)
+    pt = rng.permutation(npages)[: batch * maxp].reshape(batch, maxp).astype(np.int32)
+    return rng, K, V, pt
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_kv_write_block_flags(gpu, D):
+    rng, K, V, pt = _kv_setup(D, D=D)
+    start = np.array([0, 5, 100, 37], dtype=np.int32)       # aligned, mid-page, later, unaligned
+    lens = np.array([128, 96, 128, 64], dtype=np.int32)
+    B = 32
+    flags = np.array([[1, 0, 1, 0], [0, 1, 1, 0], [0, 0, 0, 0], [1, 1, 0, 0]], dtype=np.uint8)
+    T = int(lens.sum())
+    kn = torch.from_numpy(rng.normal(size=(T, K.shape[1], D)).astype(np.float32)).to(torch.bfloat16)
+    vn = torch.from_numpy(rng.normal(size=(T, K.shape[1], D)).astype(np.float32)).to(torch.bfloat16)
+    Kd, Vd = K.to(DEV), V.to(DEV)
+    gpu.kv_write(Kd, Vd, torch.from_numpy(pt).to(DEV), torch.from_numpy(start).to(DEV),
+                 torch.from_numpy(lens).to(DEV), kn.to(DEV), vn.to(DEV), max_len=128,
+                 block_flags=torch.from_numpy(flags).to(DEV), block_size=B)
+    torch.cuda.synchronize()
+    rk, rv = oracle.kv_write(K.view(torch.int16), V.view(torch.int16), pt, start, lens, kn.view(torch.int16),
+                             vn.view(torch.int16), block_flags=flags, block_size=B)
+    assert np.array_equal(Kd.cpu().view(torch.int16).numpy(), rk)
+    assert np.array_equal(Vd.cpu().view(torch.int16).numpy(), rv)
+
+
+def test_kv_write_skips_out_of_range_tokens(gpu):
+    """Positions past a sequence's table row, page ids outside the pool and
+    rows past total_tokens are not written anywhere (K and V alike); every
+    other token is written as the oracle writes it."""
+    rng, K, V, pt = _kv_setup(5)
+    pt = pt[:, :6].copy()                                  # 6 table pages = 96 positions per sequence
+    start = np.array([80, 0, 16, 0], dtype=np.int32)
+    lens = np.array([32, 32, 32, 32], dtype=np.int32)      # seq 0 runs past its table row (80..111)
+    pt[1, 1] = K.shape[0] + 3                              # seq 1: positions 16..31 on a page outside the pool
+    pt[2, 2] = -1                                          # seq 2: positions 32..47 on a negative page id
+    T = int(lens.sum())
+    kn = torch.from_numpy(rng.normal(size=(T, K.shape[1], 128)).astype(np.float32)).to(torch.bfloat16)
+    vn = torch.from_numpy(rng.normal(size=(T, K.shape[1], 128)).astype(np.float32)).to(torch.bfloat16)
+    total = T - 8                                          # the last 8 rows of seq 3 lie past total_tokens
+    Kd, Vd = K.to(DEV), V.to(DEV)
+    lib = gpu.load()
+    import ctypes
+    st = lib.mbe_kv_write(ctypes.c_void_p(Kd.data_ptr()), ctypes.c_void_p(Vd.data_ptr()), K.shape[0], K.shape[1],
+                          128, None, 6, None, None, 4, 32, total, None, None, None, 0, None)
+    assert st == 1                                         # NULL arguments are rejected on the host
+    ptd, sd, ld = torch.from_numpy(pt).to(DEV), torch.from_numpy(start).to(DEV), torch.from_numpy(lens).to(DEV)
+    knd, vnd = kn.to(DEV), vn.to(DEV)
+    st = lib.mbe_kv_write(ctypes.c_void_p(Kd.data_ptr()), ctypes.c_void_p(Vd.data_ptr()), K.shape[0], K.shape[1],
+                          128, ctypes.c_void_p(ptd.data_ptr()), 6, ctypes.c_void_p(sd.data_ptr()),
+                          ctypes.c_void_p(ld.data_ptr()), 4, 32, total, ctypes.c_void_p(knd.data_ptr()),
+                          ctypes.c_void_p(vnd.data_ptr()), None, 0,
+                          ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert st == 0, lib.mbe_last_error()
+    torch.cuda.synchronize()
+    # the oracle on the valid tokens only: flags mark them (block size 1)
+    valid = np.ones((4, 32), dtype=np.uint8)
+    valid[0, 96 - 80:] = 0                                  # positions 96..111: no table slot
+    valid[1, 16:32] = 0                                    # page outside the pool
+    valid[2, 32 - 16:48 - 16] = 0                          # negative page id
+    valid[3, 24:] = 0                                      # rows past total_tokens
+    ptv = np.where((pt >= 0) & (pt < K.shape[0]), pt, 0)
+    rk, rv = oracle.kv_write(K.view(torch.int16), V.view(torch.int16), ptv, start, lens, kn.view(torch.int16),
+                             vn.view(torch.int16), block_flags=valid, block_size=1)
+    assert np.array_equal(Kd.cpu().view(torch.int16).numpy(), rk)
+    assert np.array_equal(Vd.cpu().view(torch.int16).numpy(), rv)
+
+
+# ------------------------------------------------------------------ the refresh chain
+def _chain_logits(rng, rows, V, change, B):
+    """N(0, 1) logits (confidence far below 0.5) with a +12 peak in every
+    row of the blocks listed in `change`; current tokens never hit a peak."""
+    L = rng.normal(0.0, 1.0, (rows, V)).astype(np.float32)
+    cur = rng.integers(0, V - 1, rows).astype(np.int32)
+    for blk in change:
+        for r in range(blk * B, (blk + 1) * B):
+            col = int(rng.integers(0, V - 1))
+            L[r, col] = L[r].max() + 12.0
+            if cur[r] == col:
+                cur[r] = (col + 1) % (V - 1)
+    return torch.from_numpy(L).to(torch.bfloat16), torch.from_numpy(cur)
+
+
+@pytest.mark.parametrize("mode", ["changed", "changed_and_later"])
+def test_refresh_chain(gpu, mode):
+    """threshold update -> block flags -> refresh set -> block-causal
+    attention of the flagged blocks -> K/V write-back of those blocks -> next
+    window attention, all on the device with no host read in between, against
+    the same chain through the oracle."""
+    B, k = 32, 4
+    case = _attn_case(21, [900, 2000, 333, 64], k=k, B=B)
+    batch, W = case.batch, k * B
+    rng = np.random.default_rng(22)
+    change = [0 * k + 1, 2 * k + 0, 2 * k + 3, 3 * k + 2]          # (sequence, block) -> flat block ids
+    L, cur = _chain_logits(rng, batch * W, 4096, change, B)
+    kn = torch.from_numpy(rng.normal(size=(batch * W, case.num_kv_heads, case.head_dim)).astype(np.float32))
+    vn = torch.from_numpy(rng.normal(size=(batch * W, case.num_kv_heads, case.head_dim)).astype(np.float32))
+    kn, vn = kn.to(torch.bfloat16), vn.to(torch.bfloat16)
+    c = case.to(DEV)
+    q2 = torch.from_numpy(rng.normal(size=tuple(case.q.shape)).astype(np.float32)).to(torch.bfloat16)
+
+    # device chain
+    upd = gpu.threshold_update(L.to(DEV), cur.to(DEV), 4095, B, 0.5, 0.5)
+    refresh = gpu.refresh_blocks(upd["block_changed"].view(batch, k), mode)
+    out_r = torch.full_like(c.q, SENTINEL)
+    bounds = dict(max_prefix_len=int(case.prefix_lens.max()), max_window_len=W)   # no host read of device data
+    gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, B,
+                         mask_mode="block_causal", out=out_r, block_flags=refresh, **bounds)
+    gpu.kv_write(c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, kn.to(DEV), vn.to(DEV),
+                 max_len=W, block_flags=refresh, block_size=B)
+    out_n = gpu.window_attention(q2.to(DEV), c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, B,
+                                 **bounds)
+    torch.cuda.synchronize()
+
+    # oracle chain
+    ref_u = oracle.threshold_update(L, cur, 4095, B, 0.5, 0.5)
+    assert np.array_equal(upd["block_changed"].cpu().numpy(), ref_u["block_changed"])
+    want = np.zeros(batch * k, dtype=np.uint8)
+    want[change] = 1
+    assert np.array_equal(ref_u["block_changed"], want)
+    ref_f = oracle.refresh_blocks(ref_u["block_changed"].reshape(batch, k), {"changed": 0, "changed_and_later": 1}[mode])
+    assert np.array_equal(refresh.cpu().numpy(), ref_f)
+    rf = _row_flags(ref_f, case)
+    got_r = out_r.cpu()
+    assert torch.all(got_r[torch.from_numpy(~rf)] == SENTINEL)
+    ref_r = _oracle(case, "block_causal")
+    assert_attn_close(got_r[torch.from_numpy(rf)], ref_r[rf], f"refresh attention ({mode})")
+    rk, rv = oracle.kv_write(case.k_pages.view(torch.int16), case.v_pages.view(torch.int16), case.page_table,
+                             case.prefix_lens, case.window_lens, kn.view(torch.int16), vn.view(torch.int16),
+                             block_flags=ref_f, block_size=B)
+    assert np.array_equal(c.k_pages.cpu().view(torch.int16).numpy(), rk)
+    assert np.array_equal(c.v_pages.cpu().view(torch.int16).numpy(), rv)
+    case2 = synth.AttnCase(q=q2, k_pages=torch.from_numpy(rk).view(torch.bfloat16),
+                           v_pages=torch.from_numpy(rv).view(torch.bfloat16),
+                           page_table=case.page_table, prefix_lens=case.prefix_lens, window_lens=case.window_lens,
+                           block_size=B, num_q_heads=case.num_q_heads, num_kv_heads=case.num_kv_heads,
+                           head_dim=case.head_dim)
+    assert_attn_close(out_n.cpu(), _oracle(case2, "bidir"), f"next pass after refresh ({mode})")
+    say(f"  refreshed blocks {int(ref_f.sum())} of {batch * k}")
+
+
+# ------------------------------------------------------------------ the pass loop
+def test_pass_loop_graph_stops_on_device(gpu):
+    """Five passes captured as one graph.  Pass 0 edits, pass 1 changes
+    nothing, passes 2-4 would edit if they ran: after a replay the tokens,
+    counts, attention outputs and update outputs equal a host-checked eager
+    loop that stops after pass 1, and passes 2-4 wrote nothing.  Three
+    replays, with eager work and synchronisations between them."""
+    from paper_2607_22663_amd.graphs import PassLoopGraph
+    B, k, Vv = 32, 2, 4096
+    case = _attn_case(31, [400, 1300], k=k, B=B)
+    c = case.to(DEV)
+    batch, W = case.batch, k * B
+    T = batch * W
+    rng = np.random.default_rng(32)
+    g = PassLoopGraph(k_pages=c.k_pages, v_pages=c.v_pages, batch=batch, window=W, block_size=B,
+                      num_q_heads=case.num_q_heads, max_pages_per_seq=case.page_table.shape[1],
+                      max_prefix_len=int(case.prefix_lens.max()), vocab=Vv, mask_id=Vv - 1, n_passes=5,
+                      omega_mask=0.5, omega_edit=0.5)
+    g.page_table.copy_(c.page_table)
+    g.prefix_lens.copy_(c.prefix_lens)
+    L0, tok0 = _chain_logits(rng, T, Vv, [0, 3], B)
+    logits = [L0, _chain_logits(rng, T, Vv, [], B)[0]] + [_chain_logits(rng, T, Vv, [0, 1, 2, 3], B)[0]
+                                                          for _ in range(3)]
+    for i in range(5):
+        g.q[i].copy_(torch.from_numpy(rng.normal(size=tuple(case.q.shape)).astype(np.float32)).to(torch.bfloat16))
+        g.logits[i].copy_(logits[i])
+    g.capture()
+
+    # host-checked eager loop
+    def reset():
+        g.tokens.copy_(tok0)
+        g.out.fill_(SENTINEL)
+        g.conf.fill_(-1.0)
+        g.action.fill_(9)
+        g.block_changed.fill_(9)
+        g.counts.fill_(-1)
+        torch.cuda.synchronize()
+
+    reset()
+    ran = 0
+    for i in range(5):
+        g.run_eager(i)
+        ran += 1
+        if int(g.counts[i].item()) == 0:
+            break
+    assert ran == 2, ran
+    want = {n: getattr(g, n).clone() for n in ("tokens", "out", "conf", "action", "block_changed", "counts")}
+    assert int(want["counts"][0].item()) == 2 * B
+    for rep in range(3):
+        reset()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(g.tokens, want["tokens"]), rep
+        assert torch.equal(g.counts[:2], want["counts"][:2]) and torch.all(g.counts[2:] == 0), (rep, g.counts)
+        assert torch.equal(g.out[:2], want["out"][:2]) and torch.all(g.out[2:] == SENTINEL), rep
+        assert torch.equal(g.conf[:2].view(torch.int32), want["conf"][:2].view(torch.int32))
+        assert torch.all(g.conf[2:] == -1.0)
+        assert torch.equal(g.action[:2], want["action"][:2]) and torch.all(g.action[2:] == 0)
+        assert torch.equal(g.block_changed[:2], want["block_changed"][:2]) and torch.all(g.block_changed[2:] == 0)
+        _ = torch.ones(1000, device=DEV).sum().item()       # eager work between replays
+    # the tokens pass 0 wrote are the oracle's
+    ref = oracle.threshold_update(L0, tok0, Vv - 1, B, 0.5, 0.5)
+    assert np.array_equal(g.tokens.cpu().numpy(), ref["new_tokens"])
+    ref_a = oracle.window_attention(g.q[0].cpu(), case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
+                                    case.window_lens, B)
+    assert_attn_close(g.out[0].cpu(), ref_a, "pass 0 attention in the graph")
