@@ -243,6 +243,23 @@ mbe_status mbe_threshold_update(const void *logits, int64_t rows, int64_t vocab,
  * the per-chunk partials of mbe_edit_select).  (size_t)-1 for negative sizes. */
 size_t mbe_threshold_update_workspace_size(int64_t rows, int64_t vocab);
 
+/* mbe_threshold_update for callers that cannot allocate device memory and
+ * hold no workspace (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and checks as
+ * mbe_threshold_update, without the workspace: the scratch it needs (the
+ * per-row predictions and chunk partials) lives in a static 1 MiB device
+ * array inside the library, one per GPU, kept until the process ends.  Calls
+ * whose scratch (mbe_threshold_update_workspace_size(rows, vocab)) exceeds
+ * 1 MiB, i.e. beyond 262144 rows, return MBE_ERR_WORKSPACE and launch
+ * nothing.  It calls no allocator.  All calls on one GPU share its array:
+ * calls that overlap in time on one GPU (different streams or host threads)
+ * race; calls on one stream are ordered and safe. */
+mbe_status mbe_threshold_update_noalloc(const void *logits, int64_t rows, int64_t vocab, int64_t row_stride,
+                                        const int32_t *cur_tokens, int32_t mask_id, int32_t block_size,
+                                        float omega_mask, float omega_edit, int32_t *new_tokens, float *conf,
+                                        uint8_t *action, uint8_t *block_changed, int32_t *changed_count,
+                                        float *entropy, const int32_t *run_if_nonzero, void *stream);
+
 /* Tail-entropy score of every block (paper, Sec. "Training-Free MBE
  * Decoding", Eq. (5)): scores[k] = mean of the ceil(rho * block_size) largest
  * entropy values of rows k*block_size .. (k+1)*block_size - 1.  The values are

@@ -29,7 +29,8 @@ MASK_MODES = {"bidir": 0, "block_causal": 1}
 EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_attention_workspace_size",
            "mbe_block_diffusion_workspace_size", "mbe_edit_select", "mbe_edit_select_workspace_size",
            "mbe_threshold_update", "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores",
-           "mbe_select_start_block", "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error")
+           "mbe_select_start_block", "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error",
+           "mbe_threshold_update_noalloc")
 ACTIONS = {"keep": 0, "unmask": 1, "force_unmask": 2, "edit": 3}
 REFRESH_MODES = {"changed": 0, "changed_and_later": 1}
 
@@ -94,6 +95,9 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_threshold_update.argtypes = [vp, i64, i64, i64, vp, i32, i32, f32, f32, vp, vp, vp, vp, vp, vp, vp,
                                              vp, sz, vp]
         lib.mbe_threshold_update.restype = ctypes.c_int
+        lib.mbe_threshold_update_noalloc.argtypes = [vp, i64, i64, i64, vp, i32, i32, f32, f32, vp, vp, vp, vp, vp,
+                                                     vp, vp, vp]
+        lib.mbe_threshold_update_noalloc.restype = ctypes.c_int
         lib.mbe_threshold_update_workspace_size.argtypes = [i64, i64]
         lib.mbe_threshold_update_workspace_size.restype = sz
         lib.mbe_tail_entropy_scores.argtypes = [vp, i64, i32, f32, vp, vp]
@@ -423,6 +427,32 @@ def threshold_update(logits, cur_tokens, mask_id, block_size, omega_mask, omega_
         ctypes.c_float(omega_edit), _ptr(out["new_tokens"]), _ptr(out["conf"]), _ptr(out["action"]),
         _ptr(out["block_changed"]), _ptr(out.get("changed_count")), _ptr(out.get("entropy")), _ptr(run_if_nonzero),
         _ptr(ws), need if ws is not None else 0, _stream(dev)))
+    return out
+
+
+@_on_device
+def threshold_update_noalloc(logits, cur_tokens, mask_id, block_size, omega_mask, omega_edit, *, out,
+                             vocab=None, run_if_nonzero=None):
+    """threshold_update through mbe_threshold_update_noalloc: no workspace and
+    no allocation (the library's static per-GPU scratch).  `out` is the dict
+    of output tensors threshold_update returns (entropy and changed_count
+    optional); nothing is allocated here either."""
+    lib = load()
+    dev = logits.device
+    _need(cur_tokens, "cur_tokens", torch.int32, dev, 1)
+    if logits.dtype != torch.bfloat16 or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a bf16 [rows, row_stride] tensor with unit column stride")
+    rows = logits.shape[0]
+    v = logits.shape[1] if vocab is None else int(vocab)
+    if cur_tokens.shape[0] != rows or not 0 <= v <= logits.shape[1]:
+        raise ValueError("cur_tokens must have one entry per row and vocab fit the columns")
+    ld = logits.stride(0) if rows > 1 else max(logits.shape[1], 1)
+    _flags_gate(None, None, run_if_nonzero, dev)
+    _check("mbe_threshold_update_noalloc", lib.mbe_threshold_update_noalloc(
+        _ptr(logits), rows, v, ld, _ptr(cur_tokens), int(mask_id), int(block_size), ctypes.c_float(omega_mask),
+        ctypes.c_float(omega_edit), _ptr(out["new_tokens"]), _ptr(out["conf"]), _ptr(out["action"]),
+        _ptr(out["block_changed"]), _ptr(out.get("changed_count")), _ptr(out.get("entropy")), _ptr(run_if_nonzero),
+        _stream(dev)))
     return out
 
 

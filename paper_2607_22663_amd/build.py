@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmbe.so")
-SOURCES = ["abi.cpp", "edit_select.hip", "attn_window.hip", "block_select.hip", "kv_write.hip"]
+SOURCES = ["abi.cpp", "edit_select.hip", "attn_window.hip", "block_select.hip", "kv_write.hip", "noalloc.hip"]
 
 # Packed fp32 VALU ops are disabled for every HIP source: ordinary float code
 # is compiled to scalar-per-lane v_*_f32 instructions only.  MFMA results are

@@ -29,7 +29,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(mbe.EXPORTS)
@@ -346,3 +346,18 @@ def test_error_string_is_per_thread():
     for t in threads:
         t.join()
     assert not errors, errors[:3]
+
+
+def test_threshold_update_noalloc_rejects_on_the_host(lib):
+    """The no-allocation update checks its arguments like mbe_threshold_update
+    and refuses shapes whose scratch exceeds its static 1 MiB (here 262176
+    rows of predictions), before any HIP call."""
+    def call(rows, omega=0.5):
+        return lib.mbe_threshold_update_noalloc(_vp(16), rows, 16, 16, _vp(16), 15, 32, ctypes.c_float(omega),
+                                                ctypes.c_float(0.0), _vp(16), _vp(16), _vp(16), _vp(16), None, None,
+                                                None, None)
+    assert call(262176) == 4 and "scratch" in lib.mbe_last_error().decode()
+    assert lib.mbe_threshold_update_workspace_size(262144, 16) <= 1 << 20
+    assert call(64, omega=float("nan")) == 6
+    assert call(30) == 2                    # not a multiple of the block
+    assert call(0) == 0                     # nothing to do
