@@ -50,6 +50,32 @@ def attention_work(case):
     return flops, kv_bytes + qo_bytes
 
 
+RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # ~315
+
+
+def attention_kernel_name(case, mode=0, v_token_major=False, max_window=None):
+    """The window_attention_kernel<D, MODE, KS, VT> instantiation a call runs:
+    KS = 2 (two waves per 64 rows, each taking half of every key tile) when a
+    sequence has at most 128 (query head, window position) rows per KV head."""
+    G = case.num_q_heads // case.num_kv_heads
+    w = int(case.window_lens.max()) if max_window is None else max_window
+    ks = 2 if G * w <= 128 else 1
+    return f"window_attention_kernel<{case.head_dim},{mode},{ks},{int(bool(v_token_major))}>"
+
+
+def attention_roofline(flops, nbytes, seconds, kernel, traffic=None):
+    """Roofline entry of one attention call: MFMA-bound (TFLOP/s against the
+    bf16 peak) when its intensity exceeds the ridge point, else HBM-bound
+    (algorithmic GB/s against 8 TB/s)."""
+    if flops / nbytes >= RIDGE_FLOP_PER_BYTE:
+        ach, peak, unit, bound = flops / seconds / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s", "mfma"
+    else:
+        ach, peak, unit, bound = nbytes / seconds / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
+    return {"kernel": kernel, "bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": unit,
+            "frac": round(ach / peak, 4), "traffic": traffic["bytes_per_launch"] if traffic else None,
+            "traffic_detail": traffic, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+
+
 def edit_bytes(rows, vocab):
     """bf16 logits read once; current token read; new token, confidence and
     changed flag written (4 + 4 + 4 + 1 bytes per row)."""
@@ -85,12 +111,15 @@ def read_traffic_file():
     return out
 
 
-def measured_traffic(kernel, workload):
+def measured_traffic(kernel, workload, variant=None):
     """HBM bytes per launch from the committed rocprofv3 --pmc summary
-    (profiles/hbm_traffic_<workload>.txt), if it
-    was taken on the current kernel sources and this workload; else None."""
+    (profiles/hbm_traffic_<workload>.txt), if it was taken on the current
+    kernel sources, this workload and (when given) this kernel instantiation;
+    else None."""
     e = read_traffic_file().get(kernel)
     if not e or e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
+        return None
+    if variant is not None and e.get("variant") != variant:
         return None
     out = {"read_bytes": int(float(e["read_bytes"])), "write_bytes": int(float(e["write_bytes"])),
            "bytes_per_launch": int(float(e["read_bytes"]) + float(e["write_bytes"])),
@@ -128,6 +157,12 @@ def _kernel_key(name):
     return None
 
 
+def _variant(name):
+    """'window_attention_kernel<128,0,1,0>' from a demangled kernel name."""
+    m = re.search(r"(\w+_kernel<[^>]*>)", name)
+    return m.group(1).replace(" ", "") if m else None
+
+
 def summarize_pmc(dirs, workload):
     """Writes the HBM traffic summary (profiles/hbm_traffic_<workload>.txt) from
     rocprofv3 --pmc runs of this script:
@@ -153,6 +188,7 @@ def summarize_pmc(dirs, workload):
              f"-d {req_dir} -o run --output-format csv -- {cmd}"]
     scale = {}
     per_kernel = {}
+    variants = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = [r for r in _counter_rows(d) if r["Counter_Name"] == counter]
         copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
@@ -161,6 +197,7 @@ def summarize_pmc(dirs, workload):
             k = _kernel_key(r["Kernel_Name"])
             if k:
                 per_kernel.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
+                variants.setdefault(k, set()).add(_variant(r["Kernel_Name"]))
     if req_dir:
         for r in _counter_rows(req_dir):
             k = _kernel_key(r["Kernel_Name"])
@@ -177,6 +214,8 @@ def summarize_pmc(dirs, workload):
         line = (f"kernel={k} workload={workload} kernel_sha={sha} fetch_kib={f:.1f} write_kib={w:.1f} "
                 f"read_bytes={f * 1024 * scale['FETCH_SIZE']:.0f} write_bytes={w * 1024 * scale['WRITE_SIZE']:.0f} "
                 f"calibration=fetch_x{scale['FETCH_SIZE']:.3f},write_x{scale['WRITE_SIZE']:.3f}")
+        if len(variants.get(k, ())) == 1 and None not in variants[k]:
+            line += f" variant={next(iter(variants[k]))}"
         n32, n64, n128 = (avg(v, f"TCC_EA0_RDREQ_{b}_sum") for b in ("32B", "64B", "128B"))
         if n32 is not None and n64 is not None and n128 is not None:
             line += (f" rdreq_32b={n32:.0f} rdreq_64b={n64:.0f} rdreq_128b={n128:.0f} "
@@ -335,7 +374,7 @@ def _time_events(fn, n):
     return ev[0].elapsed_time(ev[1]) / n / 1e3
 
 
-def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
+def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     """Times the calls outside the timed step: the full threshold update with
     entropy on the step's logits (every 32 rows a block, 40% of rows masked),
     the K/V write-back of the window (all sequences, every window token), and
@@ -403,8 +442,10 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
         t_g = _time_events(lambda: pool.replay(nb, win), steps)
         pool_rows[f"{nb}x{win}"] = {"eager_ms": round(t_e * 1e3, 4), "graph_ms": round(t_g * 1e3, 4)}
     del pool
+    loop = bench_pass_loop(mbe, attn_case, c, logits, edit_case, V, steps)
     return {
         "graph_pool_edit_pass": pool_rows,
+        "pass_loop_graph": loop,
         "threshold_update": {"ms": round(t_upd * 1e3, 4), "rows": R, "vocab": V, "block": B,
                              "with_entropy": True, "algorithmic_mb": round(upd_bytes / 1e6, 1),
                              "gbs": round(upd_bytes / t_upd / 1e9, 1),
@@ -414,6 +455,57 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps):
         "tail_entropy_scores": {"ms": round(t_tail * 1e3, 4), "blocks": int(scores.shape[0])},
         "select_start_block": {"ms": round(t_sel * 1e3, 4), "sequences": attn_case.batch},
     }
+
+
+def bench_pass_loop(mbe, attn_case, c, logits, edit_case, V, steps):
+    """N_MBE = 5 editing passes (window attention + threshold update) of 8
+    sequences x 2 blocks captured as one graph, each pass after the first
+    gated on the previous pass's changed count.  Pass 0 edits (rows with a
+    +8 peak, omega_edit 0.5), pass 1 changes nothing (flat rows: confidence
+    1/V), passes 2-4 would edit: the replay runs two passes and skips three
+    on the device.  Timed against the two passes launched
+    eagerly, so (graph - eager) / 3 is the cost of a skipped pass."""
+    import torch
+    from paper_2607_22663_amd.graphs import PassLoopGraph
+    dev = logits.device
+    B, nb, win, n_pass = 32, 8, 64, 5
+    T = nb * win
+    planted = np.zeros(logits.shape[0], dtype=bool)
+    planted[edit_case.planted_rows] = True
+    rows_peak = torch.from_numpy(np.nonzero(planted)[0][:T]).to(dev)
+    g = PassLoopGraph(k_pages=c.k_pages, v_pages=c.v_pages, batch=nb, window=win, block_size=B,
+                      num_q_heads=attn_case.num_q_heads, max_pages_per_seq=c.page_table.shape[1],
+                      max_prefix_len=int(attn_case.prefix_lens.max()), vocab=V, mask_id=V - 1, n_passes=n_pass,
+                      omega_mask=0.5, omega_edit=0.5)
+    g.page_table.copy_(c.page_table[:nb])
+    g.prefix_lens.copy_(attn_case.prefix_lens[:nb].to(dev))
+    for i in range(n_pass):
+        g.q[i].copy_(c.q[i * T:(i + 1) * T])
+        if i == 1:
+            g.logits[i].zero_()          # flat rows: confidence 1/V, nothing to edit
+        else:
+            g.logits[i].copy_(logits[rows_peak])
+    tok0 = edit_case.cur_tokens.to(dev)[rows_peak]
+    g.capture()
+
+    def replay():
+        g.tokens.copy_(tok0)
+        g.replay()
+
+    def eager2():
+        g.tokens.copy_(tok0)
+        g.run_eager(0)
+        g.run_eager(1)
+    replay()
+    torch.cuda.synchronize()
+    ran = [int(x) for x in g.counts.cpu()]
+    t_graph = _time_events(replay, steps)
+    t_eager = _time_events(eager2, steps)
+    del g
+    return {"passes": n_pass, "changed_per_pass": ran, "graph_ms": round(t_graph * 1e3, 4),
+            "eager_two_passes_ms": round(t_eager * 1e3, 4),
+            "skipped_pass_ms": round((t_graph - t_eager) / 3 * 1e3, 4),
+            "shape": f"{nb} sequences x {win} rows, vocab {V}"}
 
 
 def bench_other_workloads(mbe, headline, steps):
@@ -454,17 +546,22 @@ def bench_other_workloads(mbe, headline, steps):
             c = case.to(dev)
             out = torch.empty_like(c.q)
             mp, mw = int(case.prefix_lens.max()), int(case.window_lens.max())
-            t, tm = timed(lambda: mbe.window_attention(
-                c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, case.block_size, out=out,
-                max_prefix_len=mp, max_window_len=mw, host_prefix_lens=case.prefix_lens,
-                host_window_lens=case.window_lens))
             flops, nbytes = attention_work(case)
             roof = min(PEAK_BF16_TFLOPS, flops / nbytes * PEAK_HBM_GBS / 1e3)
-            tf = flops / t / 1e12
-            r = {"attention": {"ms": round(t * 1e3, 4), "ms_median": round(tm * 1e3, 4), "tflops": round(tf, 2),
-                               "pct_mfma_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
-                               "roofline_tflops": round(roof, 1), "pct_of_roofline": round(100 * tf / roof, 2),
-                               "gbs": round(nbytes / t / 1e9, 1)}}
+            r = {}
+            for vt, vpages in ((False, c.v_pages), (True, c.v_pages.transpose(2, 3).contiguous())):
+                t, tm = timed(lambda: mbe.window_attention(
+                    c.q, c.k_pages, vpages, c.page_table, c.prefix_lens, c.window_lens, case.block_size, out=out,
+                    max_prefix_len=mp, max_window_len=mw, host_prefix_lens=case.prefix_lens,
+                    host_window_lens=case.window_lens))
+                tf = flops / t / 1e12
+                r["attention" if not vt else "attention_v_token_major"] = {
+                    "ms": round(t * 1e3, 4), "ms_median": round(tm * 1e3, 4), "tflops": round(tf, 2),
+                    "pct_mfma_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+                    "roofline_tflops": round(roof, 1), "pct_of_roofline": round(100 * tf / roof, 2),
+                    "gbs": round(nbytes / t / 1e9, 1),
+                    "roofline": attention_roofline(flops, nbytes, t, attention_kernel_name(case, 0, vt))}
+                del vpages
             del c, out
             if wl.edit is not None and k is None:
                 ec = synth.workload_edit(name)
@@ -478,7 +575,8 @@ def bench_other_workloads(mbe, headline, steps):
                                     "gbs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / PEAK_HBM_GBS, 2)}
                 del L, cur, eo
             res[tag] = r
-            print(f"[bench] {tag}: attention {r['attention']['ms']:.4f} ms", file=sys.stderr, flush=True)
+            print(f"[bench] {tag}: attention {r['attention']['ms']:.4f} ms (token-major V "
+                  f"{r['attention_v_token_major']['ms']:.4f} ms)", file=sys.stderr, flush=True)
     del flush
     return res
 
@@ -544,6 +642,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--k", type=int, default=None, help="window blocks (span sweep workload)")
     ap.add_argument("--kv-split-tokens", type=int, default=0)
+    ap.add_argument("--v-layout", choices=("minor", "major"), default="minor",
+                    help="V page layout of the timed step: token-minor [D][16] or token-major [16][D] (like K); "
+                         "the other layout is timed too and reported beside it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
     ap.add_argument("--no-flush", action="store_true", help="do not flush the infinity cache before each step")
@@ -595,7 +696,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     print(f"[bench] generating {args.workload} (seed {wl.seed})", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
-    attn_case = synth.workload_attention(args.workload, k_blocks=args.k)
+    vt = args.v_layout == "major"
+    attn_case = synth.workload_attention(args.workload, k_blocks=args.k, v_token_major=vt)
     edit_case = synth.workload_edit(args.workload) if wl.edit is not None else None
     print(f"[bench] generated in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
 
@@ -675,7 +777,28 @@ def main():
     attn_roof = min(PEAK_BF16_TFLOPS, flops / attn_bytes * PEAK_HBM_GBS / 1e3)
     edit_gbs = e_bytes / t_edit / 1e9 if edit_case is not None else None
 
-    traffic = measured_traffic("window_attention", args.workload)
+    # the same call with the other V page layout (same values), timed the same way
+    other_v = c.v_pages.transpose(2, 3).contiguous()
+    d_other = []
+    flush = None if args.no_flush else torch.empty(512 << 20, dtype=torch.uint8, device=dev).fill_(1)
+    for i in range(min(n, 20) + 3):
+        if flush is not None:
+            flush.view(torch.float32).sum()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mbe.window_attention(c.q, c.k_pages, other_v, c.page_table, c.prefix_lens, c.window_lens,
+                             attn_case.block_size, out=out, max_prefix_len=max_p, max_window_len=max_w,
+                             kv_split_tokens=args.kv_split_tokens, host_prefix_lens=hp, host_window_lens=hw)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if i >= 3:
+            d_other.append(e0.elapsed_time(e1) / 1e3)
+    del other_v, flush
+    t_other = float(np.mean(d_other))
+    kernel = attention_kernel_name(attn_case, 0, vt)
+    kernel_other = attention_kernel_name(attn_case, 0, not vt)
+
+    traffic = measured_traffic("window_attention", args.workload, variant=kernel)
     res = {
         "metric": METRIC,
         "value": round(100.0 * sol / t_step, 3),
@@ -699,6 +822,7 @@ def main():
             "head_dim": attn_case.head_dim, "page_size": 16, "mask": "bidirectional window",
             "edit_rows": R if edit_case is not None else 0, "vocab": V if edit_case is not None else 0,
             "kv_split_tokens": args.kv_split_tokens,
+            "v_page_layout": "token-major [16][D]" if vt else "token-minor [D][16]",
         },
         "attention": {"ms": round(t_attn * 1e3, 4), "ms_median": round(float(np.median(d_attn)) * 1e3, 4),
                       "ms_min": round(float(np.min(d_attn)) * 1e3, 4), "tflops": round(attn_tflops, 2),
@@ -706,7 +830,13 @@ def main():
                       "gflop": round(flops / 1e9, 2), "algorithmic_mb": round(attn_bytes / 1e6, 1),
                       "flop_per_byte": round(flops / attn_bytes, 1),
                       "roofline_tflops": round(attn_roof, 1),
-                      "pct_of_roofline": round(100 * attn_tflops / attn_roof, 2)},
+                      "pct_of_roofline": round(100 * attn_tflops / attn_roof, 2),
+                      "kernel": kernel},
+        "attention_other_v_layout": {"v_page_layout": "token-minor [D][16]" if vt else "token-major [16][D]",
+                                     "kernel": kernel_other, "ms": round(t_other * 1e3, 4),
+                                     "ms_median": round(float(np.median(d_other)) * 1e3, 4),
+                                     "tflops": round(flops / t_other / 1e12, 2),
+                                     "pct_mfma_peak": round(100 * flops / t_other / 1e12 / PEAK_BF16_TFLOPS, 2)},
         "cache": "cold: 512 MiB read before every step" if not args.no_flush else "warm (no flush)",
         "edit_select": ({"ms": round(t_edit * 1e3, 4), "ms_median": round(float(np.median(d_edit)) * 1e3, 4),
                          "ms_min": round(float(np.min(d_edit)) * 1e3, 4), "gbs": round(edit_gbs, 1),
@@ -714,15 +844,11 @@ def main():
                          "algorithmic_mb": round(e_bytes / 1e6, 1),
                          "traffic": measured_traffic("edit_select", args.workload)}
                         if edit_case is not None else None),
-        "roofline": {"kernel": "window_attention_kernel<128,0,1>", "bound": "mfma",
-                     "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic["bytes_per_launch"] if traffic else None,
-                     "traffic_detail": traffic, "algorithmic_bytes": attn_bytes},
+        "roofline": attention_roofline(flops, attn_bytes, t_attn, kernel, traffic),
         "wall_s": round(wall, 3),
     }
     if edit_case is not None and not args.no_next:
-        res["next_rows"] = bench_next_rows(mbe, attn_case, c, logits, cur, R, V, args.steps)
+        res["next_rows"] = bench_next_rows(mbe, attn_case, c, logits, cur, R, V, args.steps, edit_case)
     if not args.no_others:
         res["other_workloads"] = bench_other_workloads(mbe, args.workload, min(args.steps, 20))
     if not args.no_cpu_baseline and edit_case is not None:

@@ -65,9 +65,17 @@ typedef enum {
  * The two coincide when the window is one block. */
 typedef enum { MBE_MASK_WINDOW_BIDIR = 0, MBE_MASK_BLOCK_CAUSAL = 1 } mbe_mask_mode;
 
+/* Layout of the V pages (K pages are always token-major). */
+typedef enum {
+  MBE_V_TOKEN_MINOR = 0,  /* v_pages[num_pages][num_kv_heads][head_dim][16]             */
+  MBE_V_TOKEN_MAJOR = 1   /* v_pages[num_pages][num_kv_heads][16][head_dim], like K: the
+                             common paged-cache layout                                  */
+} mbe_v_layout;
+
 /* Paged KV cache for one layer.  Pages hold 16 tokens; all bf16.
  *   k_pages: [num_pages][num_kv_heads][16][head_dim]   token-major page
- *   v_pages: [num_pages][num_kv_heads][head_dim][16]   token-minor page
+ *   v_pages: as v_layout says (token-minor [head_dim][16] or token-major
+ *            [16][head_dim] per page and head)
  * Token t of sequence b is slot t % 16 of page page_table[b][t / 16].  The
  * window's own K/V (tokens P_b .. P_b+W_b-1) are read through the same table
  * from pages the caller provides.  The library only reads the cache, as the
@@ -81,6 +89,7 @@ typedef struct {
   int32_t page_size;     /* must be 16            */
   int32_t num_kv_heads;  /* Hkv >= 1              */
   int32_t head_dim;      /* D: 64 or 128          */
+  int32_t v_layout;      /* mbe_v_layout (0 = token-minor)  */
 } mbe_paged_kv;
 
 /* Options of the attention calls.  The bounds are host-side facts the caller
@@ -284,7 +293,8 @@ mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t sc
  * absolute position start_pos[b] + t, i.e. slot (position % 16) of page
  * page_table[b][position / 16], for every KV head:
  *   k_pages[page][head][slot][:] = k_new[row][head][:]      (bf16)
- *   v_pages[page][head][:][slot] = v_new[row][head][:]      (token-minor pool)
+ *   v_pages[page][head][:][slot] = v_new[row][head][:]      (v_layout MBE_V_TOKEN_MINOR)
+ *   v_pages[page][head][slot][:] = v_new[row][head][:]      (v_layout MBE_V_TOKEN_MAJOR)
  * k_new/v_new: bf16 [total_tokens][num_kv_heads][head_dim]; max_len bounds
  * every lens[b] (host-known, sizes the grid).  Other slots are not touched.
  * block_flags (device uint8, may be NULL = write every token): the targeted
@@ -296,7 +306,7 @@ mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t sc
  * sequence's table row, page ids inside the pool, sum of lens = total_tokens.
  * A token that breaks them is not written (it never lands on another slot). */
 mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads,
-                        int32_t head_dim, const int32_t *page_table, int32_t max_pages_per_seq,
+                        int32_t head_dim, int32_t v_layout, const int32_t *page_table, int32_t max_pages_per_seq,
                         const int32_t *start_pos, const int32_t *lens, int32_t batch, int32_t max_len,
                         int32_t total_tokens, const void *k_new, const void *v_new,
                         const uint8_t *block_flags, int32_t block_size, void *stream);

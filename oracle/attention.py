@@ -49,11 +49,12 @@ def _i64(x) -> np.ndarray:
     return np.asarray(x, dtype=np.int64)
 
 
-def gather_kv(k_pages, v_pages, page_table_row, n_tokens, kv_head):
+def gather_kv(k_pages, v_pages, page_table_row, n_tokens, kv_head, v_token_major=False):
     """K and V of one sequence's first n_tokens for one KV head, as [n, D].
 
     Token t lives in page page_table_row[t // 16] at slot t % 16.  K pages
-    are [num_pages, Hkv, 16, D]; V pages are [num_pages, Hkv, D, 16].
+    are [num_pages, Hkv, 16, D]; V pages are [num_pages, Hkv, D, 16]
+    (token-minor) or, with v_token_major, [num_pages, Hkv, 16, D] like K.
     """
     t = np.arange(n_tokens)
     page = np.asarray(page_table_row)[t // PAGE_SIZE]
@@ -62,7 +63,10 @@ def gather_kv(k_pages, v_pages, page_table_row, n_tokens, kv_head):
         import torch
         page, slot = torch.from_numpy(page), torch.from_numpy(slot)
     K = _f64(k_pages[page, kv_head, slot, :])    # [n, D]
-    V = _f64(v_pages[page, kv_head, :, slot])    # [n, D]
+    if v_token_major:
+        V = _f64(v_pages[page, kv_head, slot, :])
+    else:
+        V = _f64(v_pages[page, kv_head, :, slot])    # [n, D]
     return K, V
 
 
@@ -77,7 +81,7 @@ def visible_count(prefix_len, window_len, block_size, i, mask_mode):
 
 def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens,
                      block_size, mask_mode=MASK_BIDIR, softmax_scale=None,
-                     return_probs=False):
+                     return_probs=False, v_token_major=False):
     """Reference output, fp64 [total_q, Hq, D].
 
     q [total_q, Hq, D]: rows of sequence b start at sum of earlier window
@@ -103,7 +107,7 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens,
         if W == 0:
             continue
         for g in range(Hkv):
-            K, V = gather_kv(kp, vp, pt[b], n_all, g)
+            K, V = gather_kv(kp, vp, pt[b], n_all, g, v_token_major)
             for h in range(g * G, (g + 1) * G):
                 Qb = q[row0:row0 + W, h, :]                       # [W, D]
                 S = scale * (Qb @ K.T)                            # [W, n_all]
@@ -124,9 +128,9 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens,
 
 
 def block_diffusion_attention(q, k_pages, v_pages, page_table, prefix_lens, block_size,
-                              softmax_scale=None):
+                              softmax_scale=None, v_token_major=False):
     """Standard single-block step (Sec. "Block diffusion"): block j's B queries
     see the prefix x_{0:jB} and, bidirectionally, their own block."""
     W = np.full(_i64(prefix_lens).shape[0], block_size, dtype=np.int64)
     return window_attention(q, k_pages, v_pages, page_table, prefix_lens, W, block_size,
-                            MASK_BIDIR, softmax_scale)
+                            MASK_BIDIR, softmax_scale, v_token_major=v_token_major)

@@ -8,7 +8,8 @@ diffusion" and Eq. (4)): committed prefix tokens carry id -1; window token u
 (absolute position P + u) carries id u // B.  A window query of block c sees
   * bidirectional window mode: every token (ids -1 .. k-1);
   * block-causal (standard) mode: tokens whose id is <= c.
-For tiny inputs only.
+V pages are [page][head][D][16] (token-minor) or, with v_token_major,
+[page][head][16][D].  For tiny inputs only.
 """
 from __future__ import annotations
 
@@ -25,7 +26,7 @@ def _lst(x):
 
 
 def brute_window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens,
-                           block_size, bidirectional=True, softmax_scale=None):
+                           block_size, bidirectional=True, softmax_scale=None, v_token_major=False):
     q, kp, vp = _lst(q), _lst(k_pages), _lst(v_pages)
     pt, P_all, W_all = _lst(page_table), _lst(prefix_lens), _lst(window_lens)
     Hq = len(q[0]) if q else 0
@@ -61,7 +62,7 @@ def brute_window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_
                     acc = 0.0
                     for t, e in w:
                         pg, sl = pt[b][t // page], t % page
-                        acc += e * vp[pg][g][d][sl]
+                        acc += e * (vp[pg][g][sl][d] if v_token_major else vp[pg][g][d][sl])
                     out[base + u][h][d] = acc / z
         base += W
     return out

@@ -8,7 +8,8 @@ restores a cache consistent with standard-scope decoding.
 kv_write is the write-back: token t of sequence b (absolute position
 start_b + t, t < n_b) goes to slot (start_b + t) % 16 of page
 page_table[b][(start_b + t) // 16], for every KV head.  The K pool is
-[page][head][16][D]; the V pool [page][head][D][16] (token-minor).  With
+[page][head][16][D]; the V pool [page][head][D][16] (token-minor) or, with
+v_token_major, [page][head][16][D] like K.  With
 block flags ([batch][blocks], block size B), token t of sequence b is
 written only when flags[b][t // B] is set: the blocks the refresh recomputes.
 
@@ -29,7 +30,8 @@ def _np(x):
     return x.detach().cpu().numpy() if hasattr(x, "detach") else np.asarray(x)
 
 
-def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, block_flags=None, block_size=None):
+def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, block_flags=None, block_size=None,
+             v_token_major=False):
     """Returns updated copies of the two pools (same dtype as given)."""
     K = _np(k_pages).copy()
     V = _np(v_pages).copy()
@@ -47,7 +49,10 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, block_
                 page = int(pt[b, pos // PAGE])
                 slot = pos % PAGE
                 K[page, :, slot, :] = kn[row]
-                V[page, :, :, slot] = vn[row]
+                if v_token_major:
+                    V[page, :, slot, :] = vn[row]
+                else:
+                    V[page, :, :, slot] = vn[row]
             row += 1
     return K, V
 

@@ -41,10 +41,26 @@ class MbeError(RuntimeError):
         super().__init__(f"{call}: {STATUS_NAMES.get(status, status)}: {detail}")
 
 
+V_TOKEN_MINOR, V_TOKEN_MAJOR = 0, 1
+
+
 class PagedKV(ctypes.Structure):
     _fields_ = [("k_pages", ctypes.c_void_p), ("v_pages", ctypes.c_void_p),
                 ("num_pages", ctypes.c_int32), ("page_size", ctypes.c_int32),
-                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32)]
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("v_layout", ctypes.c_int32)]
+
+
+def v_layout_of(k_pages, v_pages):
+    """V_TOKEN_MAJOR when v_pages is [num_pages, Hkv, 16, D] like k_pages,
+    V_TOKEN_MINOR when it is [num_pages, Hkv, D, 16] (head_dim is never 16)."""
+    n_pages, hkv, page, d = k_pages.shape
+    if tuple(v_pages.shape) == (n_pages, hkv, page, d):
+        return V_TOKEN_MAJOR
+    if tuple(v_pages.shape) == (n_pages, hkv, d, page):
+        return V_TOKEN_MINOR
+    raise ValueError(f"v_pages must be [num_pages, Hkv, 16, D] or [num_pages, Hkv, D, 16] = "
+                     f"{(n_pages, hkv, page, d)} or {(n_pages, hkv, d, page)}, got {tuple(v_pages.shape)}")
 
 
 class AttnOpts(ctypes.Structure):
@@ -104,7 +120,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.mbe_tail_entropy_scores.restype = ctypes.c_int
         lib.mbe_select_start_block.argtypes = [vp, i32, i32, vp, i32, vp, vp]
         lib.mbe_select_start_block.restype = ctypes.c_int
-        lib.mbe_kv_write.argtypes = [vp, vp, i32, i32, i32, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp]
+        lib.mbe_kv_write.argtypes = [vp, vp, i32, i32, i32, i32, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp]
         lib.mbe_kv_write.restype = ctypes.c_int
         lib.mbe_refresh_blocks.argtypes = [vp, i32, i32, i32, vp, vp]
         lib.mbe_refresh_blocks.restype = ctypes.c_int
@@ -214,7 +230,7 @@ def workspace_bytes_window_attention(q, k_pages, page_table, batch, block_size, 
     """Workspace bytes of a window_attention call planned from bounds only
     (no host lengths), as a captured graph replays it."""
     lib = load()
-    kv = PagedKV(None, None, k_pages.shape[0], k_pages.shape[2], k_pages.shape[1], k_pages.shape[3])
+    kv = PagedKV(None, None, k_pages.shape[0], k_pages.shape[2], k_pages.shape[1], k_pages.shape[3], 0)
     opts = AttnOpts(int(batch), q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len), int(max_window_len),
                     MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode), 0.0,
                     int(kv_split_tokens), None, None, None, 0, None, None, None)
@@ -236,9 +252,7 @@ def _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out):
     _need(page_table, "page_table", torch.int32, dev, 2)
     _need(prefix_lens, "prefix_lens", torch.int32, dev, 1)
     n_pages, hkv, page, d = k_pages.shape
-    if tuple(v_pages.shape) != (n_pages, hkv, d, page):
-        raise ValueError(f"v_pages must be [num_pages, Hkv, D, 16] = {(n_pages, hkv, d, page)}, "
-                         f"got {tuple(v_pages.shape)}")
+    layout = v_layout_of(k_pages, v_pages)
     if q.shape[2] != d:
         raise ValueError(f"q head_dim {q.shape[2]} != cache head_dim {d}")
     if page_table.shape[0] != prefix_lens.shape[0]:
@@ -249,7 +263,7 @@ def _attn_common(q, k_pages, v_pages, page_table, prefix_lens, out):
         _need(out, "out", torch.bfloat16, dev, 3)
         if out.shape != q.shape:
             raise ValueError("out must have the shape of q")
-    kv = PagedKV(_ptr(k_pages), _ptr(v_pages), n_pages, page, hkv, d)
+    kv = PagedKV(_ptr(k_pages), _ptr(v_pages), n_pages, page, hkv, d, layout)
     return kv, out
 
 
@@ -280,7 +294,8 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
                      max_window_len=None, kv_split_tokens=0, host_prefix_lens=None, host_window_lens=None,
                      workspace=None, block_flags=None, run_if_nonzero=None):
     """MBE editing-window attention (paper, Sec. "Training-Free MBE Decoding",
-    Eq. (4)).  Layouts as in include/mbe.h.
+    Eq. (4)).  Layouts as in include/mbe.h; the V pool's layout is read from
+    its shape (v_layout_of).
 
     max_prefix_len / max_window_len are host-side bounds.  host_prefix_lens /
     host_window_lens are optional host copies of the lengths (they let the
@@ -490,6 +505,7 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max
              block_size=None):
     """Write recomputed K/V (bf16 [total_tokens, heads, D]) into the paged
     pools in place: token t of sequence b goes to position start_pos[b] + t.
+    The V pool's layout is read from its shape (see v_layout_of).
     block_flags: optional uint8 [batch, ceil(max_len / block_size)] device
     tensor; only tokens of flagged blocks (t // block_size) are written."""
     lib = load()
@@ -508,8 +524,9 @@ def kv_write(k_pages, v_pages, page_table, start_pos, lens, k_new, v_new, *, max
         if block_size is None or int(block_size) < 1:
             raise ValueError("block_flags needs block_size >= 1")
         _flags_gate(block_flags, (batch, -(-int(max_len) // int(block_size))), None, dev)
+    layout = v_layout_of(k_pages, v_pages)
     _check("mbe_kv_write", lib.mbe_kv_write(
-        _ptr(k_pages), _ptr(v_pages), k_pages.shape[0], k_pages.shape[1], k_pages.shape[3], _ptr(page_table),
+        _ptr(k_pages), _ptr(v_pages), k_pages.shape[0], k_pages.shape[1], k_pages.shape[3], layout, _ptr(page_table),
         page_table.shape[1], _ptr(start_pos), _ptr(lens), batch, int(max_len), k_new.shape[0], _ptr(k_new),
         _ptr(v_new), _ptr(block_flags), int(block_size or 0), _stream(dev)))
 

@@ -205,6 +205,8 @@ mbe_status plan_attention(const mbe_paged_kv *kv, const mbe_attn_opts *o, int32_
   if (kv->head_dim != 64 && kv->head_dim != 128)
     return fail(MBE_ERR_UNSUPPORTED, "head_dim %d: supported are 64 and 128", kv->head_dim);
   if (kv->num_kv_heads < 1) return fail(MBE_ERR_BAD_SHAPE, "num_kv_heads %d < 1", kv->num_kv_heads);
+  if (kv->v_layout != MBE_V_TOKEN_MINOR && kv->v_layout != MBE_V_TOKEN_MAJOR)
+    return fail(MBE_ERR_UNSUPPORTED, "v_layout %d", kv->v_layout);
   if (kv->num_pages < 0) return fail(MBE_ERR_BAD_SHAPE, "num_pages %d < 0", kv->num_pages);
   if (o->batch < 0) return fail(MBE_ERR_BAD_SHAPE, "batch %d < 0", o->batch);
   if (o->num_q_heads < 1 || o->num_q_heads % kv->num_kv_heads != 0)
@@ -498,6 +500,7 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   // at most 128 rows per (sequence, KV head): two waves per 64 rows, each
   // taking half of every key tile, instead of two waves with no rows
   p.key_split = static_cast<int64_t>(pl.group) * window_bound <= mbe::kRowsPerTile / 2 ? 2 : 1;
+  p.v_token_major = kv->v_layout == MBE_V_TOKEN_MAJOR;
   p.splits = pl.splits;
   p.kv_chunk = pl.kv_chunk;
   p.groups = pl.groups;
@@ -775,12 +778,14 @@ mbe_status mbe_select_start_block(const float *scores, int32_t batch, int32_t sc
 }
 
 mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t num_kv_heads, int32_t head_dim,
-                        const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *start_pos,
+                        int32_t v_layout, const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *start_pos,
                         const int32_t *lens, int32_t batch, int32_t max_len, int32_t total_tokens, const void *k_new,
                         const void *v_new, const uint8_t *block_flags, int32_t block_size, void *stream) {
   if (head_dim != 64 && head_dim != 128)
     return fail(MBE_ERR_UNSUPPORTED, "head_dim %d: supported are 64 and 128", head_dim);
   if (num_kv_heads < 1 || num_kv_heads > 65535) return fail(MBE_ERR_BAD_SHAPE, "num_kv_heads %d", num_kv_heads);
+  if (v_layout != MBE_V_TOKEN_MINOR && v_layout != MBE_V_TOKEN_MAJOR)
+    return fail(MBE_ERR_UNSUPPORTED, "v_layout %d", v_layout);
   if (batch < 0 || batch > 65535) return fail(MBE_ERR_BAD_SHAPE, "batch %d outside [0, 65535]", batch);
   if (max_len < 0 || total_tokens < 0 || num_pages < 0 || max_pages_per_seq < 0)
     return fail(MBE_ERR_BAD_SHAPE, "negative max_len/total_tokens/num_pages/max_pages_per_seq");
@@ -805,6 +810,7 @@ mbe_status mbe_kv_write(void *k_pages, void *v_pages, int32_t num_pages, int32_t
   p.num_pages = num_pages;
   p.num_kv_heads = num_kv_heads;
   p.head_dim = head_dim;
+  p.v_token_major = v_layout == MBE_V_TOKEN_MAJOR;
   p.page_table = page_table;
   p.max_pages = max_pages_per_seq;
   p.start_pos = start_pos;

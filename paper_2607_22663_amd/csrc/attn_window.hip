@@ -23,7 +23,10 @@
 //                  MFMA rows through a fixed permutation (swap of bits 2 and 3
 //                  of the row index) so that the 8 keys a lane contributes to
 //                  one P.V step are 8 consecutive keys: with token-minor V
-//                  pages that is one 16-byte LDS read per operand.
+//                  pages ([D][16]) that is one 16-byte LDS read per operand;
+//                  with token-major V pages ([16][D], like K) two transposing
+//                  LDS reads (ds_read_b64_tr_b16), each giving a lane 4 keys
+//                  of its dim.
 //
 // Softmax: base 2, fp32, against a fixed reference per row instead of a
 // running maximum, so inside the key loop the O accumulators are touched by
@@ -64,6 +67,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -87,6 +91,13 @@ struct Tile {
 template <int D>
 __device__ __forceinline__ int k_swz(int r) {
   return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+// LDS chunk position of global chunk j of a token-major V row r: j ^ v_swz(r).
+// A transposing read of a half-wave covers 4 consecutive key rows and 32
+// dims (4 chunks); rows r..r+3 land on disjoint 16-byte banks groups.
+template <int D>
+__device__ __forceinline__ int v_swz(int r) {
+  return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
 }
 // LDS half (16 bytes: keys 0-7 or 8-15 of a page) of half q of V dim row d.
 // The 16 lanes that LDS serves together read dims c .. c+15 of one half;
@@ -118,6 +129,16 @@ __device__ __forceinline__ bf16x8 lds_read8(const char *base, int byte_off) {
   return *reinterpret_cast<const bf16x8 *>(base + byte_off);
 }
 
+// Transposing LDS read (ds_read_b64_tr_b16): within each group of 16 lanes,
+// lane i receives element i % 4 of the 8-byte pieces that lanes i / 4,
+// i / 4 + 4, i / 4 + 8 and i / 4 + 12 address.
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x4 lds_read_tr4(const char *at) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4 *)(at));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
 typedef const __attribute__((address_space(4))) int32_t const_i32;
 
 // Page id of page `wv` of the 64-key tile starting at key0, read with a scalar
@@ -146,13 +167,24 @@ __device__ __forceinline__ void k_load_offsets(uint32_t (&koff)[Tile<D>::kLoads]
   }
 }
 
+// The same for a token-major V page: v_swz depends only on the row's low bits
+// (2 for D = 128, 3 for D = 64), which a lane keeps in every load j, so load j
+// reads lane offset + j KB.
+template <int D>
+__device__ __forceinline__ uint32_t vt_load_offset() {
+  constexpr int RC = Tile<D>::kRowChunks;
+  const int lane = threadIdx.x & 63;
+  const int row = lane / RC;
+  return static_cast<uint32_t>(row * (2 * D) + (((lane % RC) ^ v_swz<D>(row)) << 4));
+}
+
 // Issues this wave's direct HBM->LDS loads of one 64-key tile into `buf`:
 // wave wv fetches page wv of the tile, its K rows (swizzled) and its V page
 // ([D][16 keys], 8-key halves placed by v_half).  Each load reads 1 KB from
 // one page, so its address is a scalar page base plus a loop-invariant lane
 // offset (the empty asm statements keep the two apart, which selects the
 // scalar-base form of the load instead of 64-bit vector address arithmetic).
-template <int D>
+template <int D, int VT>
 __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, int pid,
                                           const uint32_t (&koff)[Tile<D>::kLoads], char *buf) {
   constexpr int PB = Tile<D>::kPageBytes;
@@ -170,11 +202,15 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + ko, (lds_void *)(kdst + j * 1024), 16,
                                      0, 0);
   }
-  // V: LDS slot j*64 + lane of the page is dim (32j + lane/2), half lane&1,
-  // and holds that dim's half v_half(d, lane & 1) (the swap is its own inverse)
+  // token-minor V: LDS slot j*64 + lane of the page is dim (32j + lane/2),
+  // half lane&1, and holds that dim's half v_half(d, lane & 1) (the swap is
+  // its own inverse).  Token-major V: rows like K, swizzled by v_swz.
   const int lane = threadIdx.x & 63;
   uint32_t vo;
-  asm("" : "=v"(vo) : "0"((lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4)), "s"(pid));
+  if constexpr (VT)
+    asm("" : "=v"(vo) : "0"(vt_load_offset<D>()), "s"(pid));
+  else
+    asm("" : "=v"(vo) : "0"((lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4)), "s"(pid));
 #pragma unroll
   for (int j = 0; j < Tile<D>::kLoads; ++j)
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + vo,
@@ -183,8 +219,14 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
 
 // Zeroes V entries of keys at or past `nvalid` (tile-relative) so that
 // unread page tails (which may hold anything) cannot reach the P.V product.
-template <int D>
+template <int D, int VT>
 __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
+  if constexpr (VT) {     // token-major: whole key rows [nvalid, 64) of the tile
+    uint4 *vs = reinterpret_cast<uint4 *>(buf + Tile<D>::kKBytes);
+    constexpr int RC = Tile<D>::kRowChunks;
+    for (int i = nvalid * RC + static_cast<int>(threadIdx.x); i < kKeyTile * RC; i += kT) vs[i] = make_uint4(0, 0, 0, 0);
+    return;
+  }
   uint16_t *vs = reinterpret_cast<uint16_t *>(buf + Tile<D>::kKBytes);
   for (int s = threadIdx.x; s < 4 * D; s += kT) {   // row s: page s / D, dim s % D, 16 keys
     const int k0 = (s / D) * kPageSize;
@@ -201,7 +243,7 @@ __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
 // sequence and KV head): waves w and w + 2 own the same 64 rows and split the
 // keys, wave w taking the first and wave w + 2 the second 32-key block of
 // every tile; their partial results are added at the end.
-template <int D, int MODE, int KS>
+template <int D, int MODE, int KS, int VT>
 __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // four K/V tile buffers (separate objects, so the compiler can tell which
   // in-flight direct loads a read depends on), three tiles in flight
@@ -329,6 +371,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int ntiles = kend > kb ? (kend - kb + kKeyTile - 1) / kKeyTile : 0;
 
   // ---- loop-invariant LDS operand offsets of this lane
+  constexpr int DB = D / 32;
   // K: row perm_row(c) (+32 for the second key block), chunk 2kk + h
   const int krow = perm_row(c);
   int koff[KK];
@@ -338,8 +381,21 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // of the page (dims 32db + c and c share the half swap, 32 being a
   // multiple of 16)
   const int voff = Tile<D>::kKBytes + c * (kPageSize * 2) + (v_half(c, h) << 4);
+  // Token-major V: transposing read q (q = 0, 1) of dim block db gives lane
+  // (c, h) dim 32db + c at keys 8h + 4q .. +3 of a 16-key step: lane l reads
+  // 4 dims (32db + 16((l >> 4) & 1) + 4(l & 3) ..) of key row 8h + (l & 15) / 4
+  // (+ 4q), the 16 lanes of a group together a 4 x 16 block.
+  int vtoff[DB];
+  if constexpr (VT) {
+    const int r = 8 * h + ((lane & 15) >> 2);                 // key row within the step, q = 0
+    const int sw = v_swz<D>(r);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int chunk = 4 * db + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+      vtoff[db] = Tile<D>::kKBytes + r * (2 * D) + ((chunk ^ sw) << 4) + 8 * (lane & 1);
+    }
+  }
 
-  constexpr int DB = D / 32;
   f32x16 acc_o[2][DB];
   float m_ref[2] = {kNegInf, kNegInf};   // reference, log2 units
   float l_run[2] = {0.f, 0.f};
@@ -360,8 +416,16 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-        va[mm][db] = lds_read8(buf, voff + (2 * kbk + mm) * Tile<D>::kPageBytes + db * 32 * (kPageSize * 2));
+      for (int db = 0; db < DB; ++db) {
+        if constexpr (VT) {
+          const char *at = buf + vtoff[db] + (2 * kbk + mm) * Tile<D>::kPageBytes;
+          const bf16x4 lo = lds_read_tr4(at);
+          const bf16x4 hi = lds_read_tr4(at + 4 * (2 * D));
+          va[mm][db] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        } else {
+          va[mm][db] = lds_read8(buf, voff + (2 * kbk + mm) * Tile<D>::kPageBytes + db * 32 * (kPageSize * 2));
+        }
+      }
   };
   // S^T of one 32-key block for both query blocks
   auto qk_mfma = [&](const bf16x8 (&a)[KK], f32x16 (&sc)[2]) {
@@ -447,7 +511,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // direct loads of tile t into dst, then the page ids of tile t + 1
   auto issue = [&](int t, char *dst) {
-    load_tile<D>(p, g, wv, pid, kload_off, dst);
+    load_tile<D, VT>(p, g, wv, pid, kload_off, dst);
     pid = wave_page(p, b, kb + (t + 1) * kKeyTile, wv);
   };
   constexpr int kLoadsPerTile = 2 * Tile<D>::kLoads;     // direct loads per thread per tile
@@ -463,7 +527,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   auto fix_tail = [&](int t) {
     const int key0 = kb + t * kKeyTile;
     if (key0 + kKeyTile > n_all) {
-      zero_v_tail<D>(buf_of(t), n_all - key0);
+      zero_v_tail<D, VT>(buf_of(t), n_all - key0);
       lds_barrier();
     }
   };
@@ -752,12 +816,14 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
 template <int D, int MODE>
 hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
   const int64_t grid = p.order_kind == kOrderUnits ? p.order_n : p.slots_per_xcd * kXcds;
-  if (p.key_split == 2)
-    hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
-                       stream, p);
-  else
-    hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1>), dim3(static_cast<unsigned>(grid)), dim3(kT), 0,
-                       stream, p);
+  const dim3 g(static_cast<unsigned>(grid)), blk(kT);
+  if (p.v_token_major) {
+    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 1>), g, blk, 0, stream, p);
+    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 1>), g, blk, 0, stream, p);
+  } else {
+    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 0>), g, blk, 0, stream, p);
+    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 0>), g, blk, 0, stream, p);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits == 1) return e;
   const int64_t items = static_cast<int64_t>(p.max_window) * p.num_q_heads * (D / 4);

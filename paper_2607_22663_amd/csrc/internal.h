@@ -27,7 +27,7 @@ enum AttnOrderKind : int32_t { kOrderNone = 0, kOrderSeqs = 1, kOrderUnits = 2 }
 struct AttnParams {
   const uint16_t *q;          // bf16 [total_q][Hq][D]
   const uint16_t *k_pages;    // bf16 [num_pages][Hkv][16][D]
-  const uint16_t *v_pages;    // bf16 [num_pages][Hkv][D][16]
+  const uint16_t *v_pages;    // bf16 [num_pages][Hkv][D][16], or [num_pages][Hkv][16][D] when v_token_major
   const int32_t *page_table;  // [batch][max_pages]
   const int32_t *prefix_lens; // [batch]
   const int32_t *window_lens; // [batch] (unused when fixed_window >= 0)
@@ -39,6 +39,7 @@ struct AttnParams {
   int32_t max_prefix, max_window;   // host-validated bounds; device lengths are clamped to them
   int32_t qtiles, splits, kv_chunk;
   int32_t key_split;          // 1, or 2 when a sequence has at most 128 rows per KV head
+  int32_t v_token_major;      // V pages [16][D] (like K) instead of [D][16]
   int64_t groups;             // (split, sequence rank, KV head) groups of qtiles work units
   int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
@@ -110,6 +111,7 @@ hipError_t launch_refresh_blocks(const uint8_t *changed, int32_t batch, int32_t 
 struct KvWriteParams {
   uint16_t *k_pages, *v_pages;
   int32_t num_pages, num_kv_heads, head_dim;
+  int32_t v_token_major;           // V pool [page][head][16][D] like K, else [page][head][D][16]
   const int32_t *page_table;
   int32_t max_pages;
   const int32_t *start_pos, *lens;

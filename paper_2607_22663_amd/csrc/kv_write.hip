@@ -10,10 +10,11 @@
 //
 // One workgroup per (sequence, page touched, KV head).  The workgroup first
 // decides which of the page's 16 slots it writes (in range, a row of the
-// input, a flagged block), then copies K rows as 16-byte chunks.  V is
-// token-minor in the pool ([D][16] per page and head): the workgroup stages
-// its tokens' V rows in LDS, then writes each dim's run of slots, 16 bytes at
-// a time where all 8 slots of a half-row are written.  A table slot past the
+// input, a flagged block), then copies K rows (and V rows of a token-major
+// pool) as 16-byte chunks.  For a token-minor V pool ([D][16] per page and
+// head) the workgroup stages its tokens' V rows in LDS, then writes each
+// dim's run of slots, 16 bytes at a time where all 8 slots of a half-row are
+// written.  A table slot past the
 // row or a page id outside the pool writes nothing.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -55,17 +56,20 @@ __global__ __launch_bounds__(256) void kv_write_kernel(KvWriteParams p) {
   const int64_t page_base = (static_cast<int64_t>(pid) * p.num_kv_heads + g) * kPageSize * D;   // elements
   const int chunks = D / 8;
   const int n = p1 - p0;
-  // K: [slot][D], a 16-byte chunk per thread; V rows staged in LDS as [slot][D]
+  // K: [slot][D], a 16-byte chunk per thread.  V: the same when the pool is
+  // token-major; otherwise its rows are staged in LDS as [slot][D]
   for (int i = threadIdx.x; i < n * chunks; i += 256) {
     const int tok = i / chunks, c = i % chunks;
     const int slot = (p0 + tok) % kPageSize;
     if (!((wmask >> slot) & 1u)) continue;
     const int64_t row = row0 + (p0 - start) + tok;
     const uint4 wk = *reinterpret_cast<const uint4 *>(p.k_new + (row * p.num_kv_heads + g) * D + c * 8);
+    const uint4 wv = *reinterpret_cast<const uint4 *>(p.v_new + (row * p.num_kv_heads + g) * D + c * 8);
     *reinterpret_cast<uint4 *>(p.k_pages + page_base + slot * D + c * 8) = wk;
-    *reinterpret_cast<uint4 *>(vs + slot * D + c * 8) =
-        *reinterpret_cast<const uint4 *>(p.v_new + (row * p.num_kv_heads + g) * D + c * 8);
+    if (p.v_token_major) *reinterpret_cast<uint4 *>(p.v_pages + page_base + slot * D + c * 8) = wv;
+    else *reinterpret_cast<uint4 *>(vs + slot * D + c * 8) = wv;
   }
+  if (p.v_token_major) return;
   __syncthreads();
   // V: [D][slot], per (dim, half of 8 slots)
   for (int i = threadIdx.x; i < D * 2; i += 256) {

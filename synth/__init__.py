@@ -14,7 +14,9 @@ Layouts produced (all row-major, contiguous):
   q          bf16  [total_q, num_q_heads, head_dim]       window rows of seq b
                                                           start at cu_q[b]
   k_pages    bf16  [num_pages, num_kv_heads, 16, head_dim]  token-major page
-  v_pages    bf16  [num_pages, num_kv_heads, head_dim, 16]  token-minor page
+  v_pages    bf16  [num_pages, num_kv_heads, head_dim, 16]  token-minor page, or
+                   [num_pages, num_kv_heads, 16, head_dim]  with v_token_major
+                   (the same values, each page transposed)
   page_table int32 [batch, max_pages_per_seq]            unused slots hold 0
   prefix_lens, window_lens int32 [batch]
   logits     bf16  [rows, vocab]
@@ -142,6 +144,10 @@ class AttnCase:
     head_dim: int
 
     @property
+    def v_token_major(self) -> bool:
+        return tuple(self.v_pages.shape[2:]) == (PAGE_SIZE, self.head_dim) and self.head_dim != PAGE_SIZE
+
+    @property
     def batch(self) -> int:
         return int(self.prefix_lens.numel())
 
@@ -170,7 +176,7 @@ def draw_prefix_lens(rng: np.random.Generator, spec: AttnSpec) -> np.ndarray:
 def make_attention_case(spec: AttnSpec, seed: int, *,
                         prefix_lens=None, window_lens=None,
                         q_scale: float = 1.0, extra_pages: int = 0,
-                        tail_fill: Optional[float] = None) -> AttnCase:
+                        tail_fill: Optional[float] = None, v_token_major: bool = False) -> AttnCase:
     """Draw one paged-KV attention case.
 
     prefix_lens / window_lens override the spec's lengths (window lengths must
@@ -179,6 +185,7 @@ def make_attention_case(spec: AttnSpec, seed: int, *,
     pool.  tail_fill, if given, overwrites every pool slot that no sequence
     references (the tail of each sequence's last page and the extra pages)
     with that value, e.g. NaN, to show those slots are never read.
+    v_token_major lays V out like K ([page, head, 16, D]) with the same values.
     """
     rng = _rng(seed, 0)
     drawn = draw_prefix_lens(rng, spec)
@@ -216,6 +223,8 @@ def make_attention_case(spec: AttnSpec, seed: int, *,
         vf[unused.unsqueeze(1).unsqueeze(2).expand_as(vf)] = tail_fill
         k_pages = kf.to(torch.bfloat16)
         v_pages = vf.to(torch.bfloat16)
+    if v_token_major:
+        v_pages = v_pages.transpose(2, 3).contiguous()
     return AttnCase(q=q, k_pages=k_pages, v_pages=v_pages,
                     page_table=torch.from_numpy(page_table),
                     prefix_lens=torch.from_numpy(P.copy()),

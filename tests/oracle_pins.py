@@ -13,7 +13,8 @@ Attention pins (paper, Sec. "Block diffusion" and Eq. (4)):
   invariance to a consistent page permutation, GQA == MHA with repeated KV
   heads, invariance to a consistent permutation of prefix keys (bidirectional);
   closed forms: V constant -> output is that constant; q = 0 -> mean of V;
-  hand-derived fixtures in tests/golden.
+  hand-derived fixtures in tests/golden; a token-major V pool against SDPA
+  over a plain-loop gather of the same values.
 Edit-selection pins (Eq. (1)):
   first-occurrence argmax by a scalar loop; confidence == max of
   scipy.special.softmax; constant rows -> (0, 1/V); ties -> lower index;
@@ -298,7 +299,30 @@ def check_golden_attention(impl):
         assert_close(o[:, 0, :want.shape[1]], want, 1e-14, f"golden attention {mode_name}")
 
 
-ATTENTION_CHECKS = [check_k1_is_block_diffusion, check_block_causal_is_stacked_blocks,
+def check_token_major_v(impl):
+    """A token-major V pool ([page][head][16][D]: the token-minor pool
+    transposed per page) gives torch fp64 SDPA over the keys and values that a
+    plain loop gathers from the token-minor pool.  head_dim 16 makes both pool
+    shapes equal, so reading one layout as the other gives wrong values
+    instead of a shape error."""
+    case = small_case(31, k=2, Hq=4, Hkv=2, D=16, prefix=(24, 7))
+    vt = case.v_pages.transpose(2, 3).contiguous()
+    G = case.num_q_heads // case.num_kv_heads
+    for mode in (impl.MASK_BIDIR, impl.MASK_BLOCK_CAUSAL):
+        o = impl.window_attention(case.q, case.k_pages, vt, case.page_table, case.prefix_lens, case.window_lens,
+                                  case.block_size, mode, v_token_major=True)
+        cu = case.cu_q
+        for b in range(case.batch):
+            P, W = int(case.prefix_lens[b]), int(case.window_lens[b])
+            ids = torch.cat([torch.full((P,), -1), torch.arange(W) // case.block_size])
+            mask = (ids[None, :] <= ids[P:, None]) | (mode == impl.MASK_BIDIR)
+            for h in range(case.num_q_heads):
+                K, V = loop_gather(case, b, h // G, P + W)
+                ref = sdpa(q_rows(case, b)[:, h], K, V, mask)
+                assert_close(o[cu[b]:cu[b + 1], h], ref.numpy(), 1e-12, f"token-major V, seq {b} head {h}")
+
+
+ATTENTION_CHECKS = [check_token_major_v, check_k1_is_block_diffusion, check_block_causal_is_stacked_blocks,
                     check_full_window_is_dense, check_prefix_and_window_is_sdpa, check_probs_normalised,
                     check_invariances,
                     check_closed_forms, check_golden_attention]

@@ -253,23 +253,27 @@ def check_kv_write_golden(kv):
     rows = int(sum(fx["lens"]))
     kn = np.array([[[(r + 1) * 10.0 + g] * D for g in range(H)] for r in range(rows)])
     vn = -kn
-    for flags, want in ((None, fx["written_row_page_slot"]), (fx["block_flags"], fx["written_with_flags"])):
+    cases = [(flags, want, vt) for flags, want in ((None, fx["written_row_page_slot"]),
+                                                    (fx["block_flags"], fx["written_with_flags"]))
+             for vt in (False, True)]
+    for flags, want, vt in cases:
         K0 = np.full((npg, H, 16, D), 0.5)
-        V0 = np.full((npg, H, D, 16), 0.5)
+        V0 = np.full((npg, H, 16, D) if vt else (npg, H, D, 16), 0.5)
         kw = {} if flags is None else {"block_flags": np.array(flags, dtype=np.uint8),
                                         "block_size": fx["flags_block_size"]}
         K, V = kv.kv_write(K0, V0, np.array(fx["page_table"]), np.array(fx["start_pos"]), np.array(fx["lens"]),
-                           kn, vn, **kw)
+                           kn, vn, v_token_major=vt, **kw)
+        Vs = V if vt else np.swapaxes(V, 2, 3)        # [page][head][slot][D] view for the checks
         hit = np.zeros((npg, 16), dtype=bool)
         for r, page, slot in want:
             hit[page, slot] = True
             for g in range(H):
                 assert np.all(K[page, g, slot, :] == kn[r, g]), (r, page, slot, K[page, g, slot])
-                assert np.all(V[page, g, :, slot] == vn[r, g]), (r, page, slot, V[page, g, :, slot])
+                assert np.all(Vs[page, g, slot, :] == vn[r, g]), (r, page, slot, Vs[page, g, slot])
         for page in range(npg):
             for slot in range(16):
                 if not hit[page, slot]:
-                    assert np.all(K[page, :, slot, :] == 0.5) and np.all(V[page, :, :, slot] == 0.5), (page, slot)
+                    assert np.all(K[page, :, slot, :] == 0.5) and np.all(Vs[page, :, slot, :] == 0.5), (page, slot)
 
 
 def check_kv_write_round_trip(kv):
@@ -294,24 +298,31 @@ def check_kv_write_round_trip(kv):
     pt[1, :need[1]] = perm[need[0]:need[0] + need[1]]
     Kc = [rng.normal(size=(int(n[b]), Hkv, D)) for b in range(2)]
     Vc = [rng.normal(size=(int(n[b]), Hkv, D)) for b in range(2)]
-    K = np.full((npg, Hkv, 16, D), np.nan)
-    V = np.full((npg, Hkv, D, 16), np.nan)
-    # prefix tokens of both sequences, then the windows from position P_b
-    K, V = kv.kv_write(K, V, pt, np.zeros(2, dtype=np.int64), P, np.concatenate([Kc[b][:P[b]] for b in range(2)]),
-                       np.concatenate([Vc[b][:P[b]] for b in range(2)]))
-    K, V = kv.kv_write(K, V, pt, P, W, np.concatenate([Kc[b][P[b]:] for b in range(2)]),
-                       np.concatenate([Vc[b][P[b]:] for b in range(2)]))
+    q = rng.normal(size=(int(W.sum()), Hq, D))
+    for vt in (False, True):
+        K = np.full((npg, Hkv, 16, D), np.nan)
+        V = np.full((npg, Hkv, 16, D) if vt else (npg, Hkv, D, 16), np.nan)
+        # prefix tokens of both sequences, then the windows from position P_b
+        K, V = kv.kv_write(K, V, pt, np.zeros(2, dtype=np.int64), P,
+                           np.concatenate([Kc[b][:P[b]] for b in range(2)]),
+                           np.concatenate([Vc[b][:P[b]] for b in range(2)]), v_token_major=vt)
+        K, V = kv.kv_write(K, V, pt, P, W, np.concatenate([Kc[b][P[b]:] for b in range(2)]),
+                           np.concatenate([Vc[b][P[b]:] for b in range(2)]), v_token_major=vt)
+        _round_trip_reads(oracle, K, V, pt, P, W, B, G, Hq, D, Kc, Vc, q, vt)
+
+
+def _round_trip_reads(oracle, K, V, pt, P, W, B, G, Hq, D, Kc, Vc, q, vt):
+    import torch
     q0 = np.zeros((int(W.sum()), Hq, D))
-    out = np.array(oracle.brute_window_attention(q0, K, V, pt, P, W, B, bidirectional=True))
+    out = np.array(oracle.brute_window_attention(q0, K, V, pt, P, W, B, bidirectional=True, v_token_major=vt))
     row = 0
     for b in range(2):
         for i in range(int(W[b])):
             for h in range(Hq):
                 assert np.allclose(out[row + i, h], Vc[b][:, h // G].mean(axis=0), rtol=0, atol=1e-12)
         row += int(W[b])
-    q = rng.normal(size=(int(W.sum()), Hq, D))
     for bidir in (True, False):
-        out = np.array(oracle.brute_window_attention(q, K, V, pt, P, W, B, bidirectional=bidir))
+        out = np.array(oracle.brute_window_attention(q, K, V, pt, P, W, B, bidirectional=bidir, v_token_major=vt))
         row = 0
         for b in range(2):
             ids = np.concatenate([np.full(P[b], -1), np.arange(W[b]) // B])

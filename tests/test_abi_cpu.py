@@ -35,8 +35,8 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(mbe.EXPORTS)
 
 
-def _kv(head_dim=128, page=16, hkv=4, pages=10):
-    return mbe.PagedKV(ctypes.c_void_p(16), ctypes.c_void_p(32), pages, page, hkv, head_dim)
+def _kv(head_dim=128, page=16, hkv=4, pages=10, v_layout=0):
+    return mbe.PagedKV(ctypes.c_void_p(16), ctypes.c_void_p(32), pages, page, hkv, head_dim, v_layout)
 
 
 def _opts(**kw):
@@ -57,6 +57,7 @@ def _attn(lib, kv, opts, B=32, q=16, out=48):
 @pytest.mark.parametrize("kv_kw,opt_kw,B,status,text", [
     (dict(head_dim=96), {}, 32, 3, "head_dim"),
     (dict(page=32), {}, 32, 3, "page_size"),
+    (dict(v_layout=2), {}, 32, 3, "v_layout"),
     ({}, dict(num_q_heads=6), 32, 2, "multiple"),
     ({}, dict(max_window_len=48), 32, 2, "multiple of block_size"),
     ({}, dict(max_pages_per_seq=0), 32, 2, "max_pages_per_seq"),
@@ -250,12 +251,14 @@ def test_select_start_validation(lib, args, status, text):
     (dict(v_pages=24), 2, "aligned"),
     (dict(num_pages=0), 2, "empty"),
     (dict(flags=16, block_size=0), 2, "block_size"),
+    (dict(v_layout=-1), 3, "v_layout"),
 ])
 def test_kv_write_validation(lib, args, status, text):
     a = dict(k_pages=16, v_pages=32, num_pages=10, heads=4, head_dim=128, pt=16, max_pages=8, start=16, lens=16,
-             batch=2, max_len=64, total=96, k_new=16, v_new=16, flags=None, block_size=0)
+             batch=2, max_len=64, total=96, k_new=16, v_new=16, flags=None, block_size=0, v_layout=0)
     a.update(args)
     st = lib.mbe_kv_write(_vp(a["k_pages"]), _vp(a["v_pages"]), a["num_pages"], a["heads"], a["head_dim"],
+                          a["v_layout"],
                           _vp(a["pt"]), a["max_pages"], _vp(a["start"]), _vp(a["lens"]), a["batch"], a["max_len"],
                           a["total"], _vp(a["k_new"]), _vp(a["v_new"]), _vp(a["flags"]), a["block_size"], None)
     assert st == status and text in lib.mbe_last_error().decode()

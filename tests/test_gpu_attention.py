@@ -31,22 +31,29 @@ def run_case(mbe, case, mode="bidir", **kw):
 def oracle_case(case, mode="bidir"):
     m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
     return oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table,
-                                   case.prefix_lens, case.window_lens, case.block_size, m)
+                                   case.prefix_lens, case.window_lens, case.block_size, m,
+                                   v_token_major=case.v_token_major)
 
 
+# both V page layouts: token-minor [D][16] and token-major [16][D] (like K)
+layouts = pytest.mark.parametrize("vt", [False, True], ids=["v_minor", "v_major"])
+
+
+@layouts
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
 @pytest.mark.parametrize("name", ["tiny_p64_k2_h4_d64", "single_p2048_k2_gqa16x4_d128"])
-def test_workload_full_parity(gpu, name, mode):
-    case = synth.workload_attention(name)
+def test_workload_full_parity(gpu, name, mode, vt):
+    case = synth.workload_attention(name, v_token_major=vt)
     say(f"  workload {name} mode {mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
     out = run_case(gpu, case, mode)
     err = assert_attn_close(out, oracle_case(case, mode), f"{name} {mode}")
     say(f"  max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
 
 
+@layouts
 @pytest.mark.parametrize("split", [64, 128, 1024])
-def test_forced_split_kv(gpu, split):
-    case = synth.workload_attention("single_p2048_k2_gqa16x4_d128")
+def test_forced_split_kv(gpu, split, vt):
+    case = synth.workload_attention("single_p2048_k2_gqa16x4_d128", v_token_major=vt)
     say(f"  kv_split_tokens {split}")
     out = run_case(gpu, case, "bidir", kv_split_tokens=split)
     assert_attn_close(out, oracle_case(case), f"split {split}")
@@ -54,14 +61,15 @@ def test_forced_split_kv(gpu, split):
 
 @pytest.mark.parametrize("nsplit", [2, 3, 5, 8, 9, 16, 17, 32, 33, 40])
 def test_merge_chunk_boundaries(gpu, nsplit):
+    vt = nsplit % 2 == 1            # both V layouts over the split counts
     """Split counts on both sides of the merge's chunk sizes (16, 8, 4, 2, 1):
     a 64-key split over P + W = 64 * nsplit - 8 keys, with a ragged second
     sequence of fewer splits and one whose window is empty."""
     spec = synth.AttnSpec(3, 16, 2, ("fixed", 0), 8, 2, 64)
     P0 = 64 * nsplit - 8 - 32
     case = synth.make_attention_case(spec, 90 + nsplit, prefix_lens=[P0, max(0, P0 // 3), 100],
-                                     window_lens=[32, 16, 0], tail_fill=float("nan"))
-    say(f"  nsplit {nsplit} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
+                                     window_lens=[32, 16, 0], tail_fill=float("nan"), v_token_major=vt)
+    say(f"  nsplit {nsplit} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()} v_token_major={vt}")
     for mode in ("bidir", "block_causal"):
         out = run_case(gpu, case, mode, kv_split_tokens=64)
         assert_attn_close(out, oracle_case(case, mode), f"nsplit {nsplit} {mode}")
@@ -80,41 +88,44 @@ def test_prefix_of_140k_keys(gpu, split):
         assert_attn_close(out, oracle_case(case, mode), f"split {split} {mode}")
 
 
+@layouts
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
-def test_ragged_batch_with_poisoned_tails(gpu, D, mode):
+def test_ragged_batch_with_poisoned_tails(gpu, D, mode, vt):
     spec = synth.AttnSpec(4, 32, 1, ("fixed", 0), 8, 2, D)
     case = synth.make_attention_case(spec, 21, prefix_lens=[0, 37, 1000, 333],
                                      window_lens=[32, 96, 64, 0], extra_pages=3,
-                                     tail_fill=float("nan"))
+                                     tail_fill=float("nan"), v_token_major=vt)
     say(f"  D={D} mode={mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
     for split in (0, 64, 256):
         out = run_case(gpu, case, mode, kv_split_tokens=split)
         assert_attn_close(out, oracle_case(case, mode), f"ragged D={D} {mode} split={split}")
 
 
+@layouts
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
-def test_key_split_waves_ragged(gpu, D, mode):
+def test_key_split_waves_ragged(gpu, D, mode, vt):
     """At most 128 rows per (sequence, KV head) (here 2 query heads per KV head,
     windows up to 64): pairs of waves split every key tile and add their
     partial results.  Ragged prefixes, an empty window, poisoned page tails."""
     spec = synth.AttnSpec(4, 32, 1, ("fixed", 0), 8, 4, D)
     case = synth.make_attention_case(spec, 31, prefix_lens=[0, 45, 1300, 211],
                                      window_lens=[64, 32, 64, 0], extra_pages=2,
-                                     tail_fill=float("nan"))
+                                     tail_fill=float("nan"), v_token_major=vt)
     say(f"  D={D} mode={mode} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()}")
     for split in (0, 64, 320):
         out = run_case(gpu, case, mode, kv_split_tokens=split)
         assert_attn_close(out, oracle_case(case, mode), f"key split D={D} {mode} split={split}")
 
 
-def test_key_split_waves_sharp_scores(gpu):
+@layouts
+def test_key_split_waves_sharp_scores(gpu, vt):
     """Single-block windows with 16 query / 4 KV heads (128 rows: the key-split
     path) and Q scaled by 8: scores spread over tens of log2 units, so later
     keys exceed the first block's maximum (the fixed softmax reference)."""
     spec = synth.AttnSpec(3, 32, 1, ("fixed", 0), 16, 4, 128)
-    case = synth.make_attention_case(spec, 41, prefix_lens=[2000, 64, 777], q_scale=8.0)
+    case = synth.make_attention_case(spec, 41, prefix_lens=[2000, 64, 777], q_scale=8.0, v_token_major=vt)
     for split in (0, 256):
         out = run_case(gpu, case, "bidir", kv_split_tokens=split)
         assert_attn_close(out, oracle_case(case), f"key split sharp split={split}")
@@ -147,14 +158,15 @@ def _plant_hot_keys(case, seed, q_gain=6.0, hot_per_seq=5):
     return case
 
 
+@layouts
 @pytest.mark.parametrize("W", [32, 64])
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
-def test_overflow_rerun(gpu, W, mode):
+def test_overflow_rerun(gpu, W, mode, vt):
     """Row sums against the first block's maximum overflow: the exact rerun
     (max-only pass, then the full pass with the true maximum) must reproduce
     the oracle.  W = 32 is the key-split path (128 rows), W = 64 the other."""
     spec = synth.AttnSpec(3, 32, W // 32, ("fixed", 0), 16, 4, 128)
-    case = synth.make_attention_case(spec, 51, prefix_lens=[700, 3000, 96])
+    case = synth.make_attention_case(spec, 51, prefix_lens=[700, 3000, 96], v_token_major=vt)
     case = _plant_hot_keys(case, 52)
     say(f"  W={W} mode={mode} P={case.prefix_lens.tolist()}")
     for split in (0, 256):
@@ -165,7 +177,7 @@ def test_overflow_rerun(gpu, W, mode):
 @pytest.mark.parametrize("B", [8, 16])
 def test_small_blocks_block_causal(gpu, B):
     spec = synth.AttnSpec(2, B, 4, ("fixed", 0), 4, 4, 128)
-    case = synth.make_attention_case(spec, 5, prefix_lens=[200, 13])
+    case = synth.make_attention_case(spec, 5, prefix_lens=[200, 13], v_token_major=B == 16)
     say(f"  block_size {B}")
     for mode in ("bidir", "block_causal"):
         out = run_case(gpu, case, mode, kv_split_tokens=128)
@@ -182,14 +194,15 @@ def test_sharp_scores_online_softmax(gpu):
         assert_attn_close(out, oracle_case(case), f"sharp split={split}")
 
 
-def test_block_diffusion_baseline(gpu):
+@layouts
+def test_block_diffusion_baseline(gpu, vt):
     spec = synth.AttnSpec(3, 32, 1, ("fixed", 0), 16, 4, 128)
-    case = synth.make_attention_case(spec, 9, prefix_lens=[640, 0, 96])
+    case = synth.make_attention_case(spec, 9, prefix_lens=[640, 0, 96], v_token_major=vt)
     c = case.to(DEV)
     out = gpu.block_diffusion_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, 32)
     torch.cuda.synchronize()
     ref = oracle.block_diffusion_attention(case.q, case.k_pages, case.v_pages, case.page_table,
-                                           case.prefix_lens, 32)
+                                           case.prefix_lens, 32, v_token_major=vt)
     assert_attn_close(out.cpu(), ref, "block_diffusion_attention")
     # k = 1: window bidirectional == block-causal == baseline, on the GPU path itself
     w_bi = run_case(gpu, case, "bidir")
@@ -207,7 +220,7 @@ def test_block_diffusion_ragged_prefixes(gpu):
                                         host_prefix_lens=case.prefix_lens)
     torch.cuda.synchronize()
     ref = oracle.block_diffusion_attention(case.q, case.k_pages, case.v_pages, case.page_table,
-                                           case.prefix_lens, 32)
+                                           case.prefix_lens, 32, v_token_major=case.v_token_major)
     assert_attn_close(out.cpu(), ref, "block_diffusion_attention, ragged prefixes")
 
 
@@ -242,7 +255,8 @@ def test_workspace_reuse_across_shapes(gpu):
         out = run_case(gpu, case, "bidir", kv_split_tokens=split)
         for b in (1, 7):
             q, pt, P, W, rows = seq_slice(case, b)
-            ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size)
+            ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size,
+                                          v_token_major=case.v_token_major)
             assert_attn_close(out[rows], ref, f"k={k} split={split} seq {b}")
 
 
@@ -272,54 +286,67 @@ def test_deterministic(gpu):
 
 
 # ---------------------------------------------------------------- benchmark sizes, every sequence
+_ORACLE_ROWS = {}     # (workload, mode, sequence) -> oracle rows; the same values in both V layouts
+
+
 def _per_sequence_parity(gpu, case, seqs, what, mode="bidir", **kw):
     """One call over the whole batch at its benchmark shape (the launch the
     bench times); the oracle then runs sequence by sequence on the rows of
-    `seqs` (every sequence unless a subset is given)."""
+    `seqs` (every sequence unless a subset is given).  Both V layouts hold
+    the same values, so the oracle rows of a sequence are computed once."""
     out = run_case(gpu, case, mode, **kw)
     m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
     worst = (0.0, 0.0)
     for b in seqs:
         q, pt, P, W, rows = seq_slice(case, b)
-        ref = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size, m)
-        err = assert_attn_close(out[rows], ref, f"{what} {mode} seq {b}")
+        key = (what, mode, b)
+        if key not in _ORACLE_ROWS:
+            _ORACLE_ROWS[key] = oracle.window_attention(q, case.k_pages, case.v_pages, pt, P, W, case.block_size, m,
+                                                        v_token_major=case.v_token_major)
+        err = assert_attn_close(out[rows], _ORACLE_ROWS[key], f"{what} {mode} seq {b} v_token_major={case.v_token_major}")
         worst = (max(worst[0], err[0]), max(worst[1], err[1]))
         say(f"  {what} {mode} seq {b} P={int(P[0])}: max_abs {err[0]:.2e} rel_rms {err[1]:.2e}")
-    say(f"  {what} {mode}: {len(seqs)} sequences, worst max_abs {worst[0]:.2e} rel_rms {worst[1]:.2e}")
+    say(f"  {what} {mode} v_token_major={case.v_token_major}: {len(seqs)} sequences, "
+        f"worst max_abs {worst[0]:.2e} rel_rms {worst[1]:.2e}")
 
 
-def test_batch32_every_sequence(gpu):
-    case = synth.workload_attention("batch32_p512to8192_k2")
+@layouts
+def test_batch32_every_sequence(gpu, vt):
+    case = synth.workload_attention("batch32_p512to8192_k2", v_token_major=vt)
     _per_sequence_parity(gpu, case, range(case.batch), "batch32")
 
 
+@layouts
 @pytest.mark.parametrize("k", synth.SPAN_SWEEP_K)
-def test_span_sweep_every_sequence(gpu, k):
-    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=k)
+def test_span_sweep_every_sequence(gpu, k, vt):
+    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=k, v_token_major=vt)
     _per_sequence_parity(gpu, case, range(case.batch), f"span k={k}")
 
 
-def test_long_context_every_sequence(gpu):
+@layouts
+def test_long_context_every_sequence(gpu, vt):
     """All 64 sequences of the long-context workload (prefixes 4K-32K, 4-block
     windows) against the oracle."""
-    case = synth.workload_attention("long_context_b64_p4096to32768_k4")
+    case = synth.workload_attention("long_context_b64_p4096to32768_k4", v_token_major=vt)
     _per_sequence_parity(gpu, case, range(case.batch), "long_context")
 
 
-def test_long_context_block_causal_sampled(gpu):
+@layouts
+def test_long_context_block_causal_sampled(gpu, vt):
     """Block-causal (the refresh scope) at the long-context shape, 4 blocks of
     32 with prefixes up to 32K: the longest, the shortest and two other
     sequences against the oracle (the launch covers all 64)."""
-    case = synth.workload_attention("long_context_b64_p4096to32768_k4")
+    case = synth.workload_attention("long_context_b64_p4096to32768_k4", v_token_major=vt)
     P = case.prefix_lens.numpy()
     seqs = sorted({int(np.argmax(P)), int(np.argmin(P)), 9, 40})
     _per_sequence_parity(gpu, case, seqs, "long_context", mode="block_causal")
 
 
-def test_span_sweep_block_causal_k4_split(gpu):
+@layouts
+def test_span_sweep_block_causal_k4_split(gpu, vt):
     """Block-causal with 4 blocks over a 16K prefix and forced 1024-key
     splits (the split-KV merge under the block-causal mask), every sequence."""
-    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=4)
+    case = synth.workload_attention("span_sweep_b8_p16384", k_blocks=4, v_token_major=vt)
     _per_sequence_parity(gpu, case, range(case.batch), "span k=4 split 1024", mode="block_causal",
                          kv_split_tokens=1024)
 
@@ -423,13 +450,14 @@ def test_pool_beyond_2_31_elements(gpu):
     torch.cuda.empty_cache()
 
 
+@layouts
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
-def test_dispatch_table_ragged_windows(gpu, mode):
+def test_dispatch_table_ragged_windows(gpu, mode, vt):
     """A small ragged batch with host lengths takes the host-placed dispatch
     table; with 8 query heads per KV head and windows of 1 to 4 blocks the
     sequences have 1 or 2 query tiles, the table's general ordering path."""
     spec = synth.AttnSpec(5, 16, 4, ("fixed", 0), 16, 2, 64)
     case = synth.make_attention_case(spec, 57, prefix_lens=[100, 3000, 700, 1500, 50],
-                                     window_lens=[16, 64, 32, 48, 0], tail_fill=float("nan"))
+                                     window_lens=[16, 64, 32, 48, 0], tail_fill=float("nan"), v_token_major=vt)
     out = run_case(gpu, case, mode, host_prefix_lens=case.prefix_lens, host_window_lens=case.window_lens)
     assert_attn_close(out, oracle_case(case, mode), f"dispatch table, ragged windows, {mode}")

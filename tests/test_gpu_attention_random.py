@@ -7,7 +7,7 @@ mode, a split-KV chunk (library's choice or forced), host lengths or bounds
 only, and extra unreferenced pages; every pool slot no sequence covers holds
 NaN.  Together the draws reach every kernel variant: one or two waves per 64
 rows (at most 128 rows per KV head), one to four query tiles per KV head,
-split and unsplit, masked tails.
+split and unsplit, masked tails.  Odd seeds use token-major V pages.
 """
 import numpy as np
 import pytest
@@ -38,7 +38,7 @@ def draw(seed):
     extra = int(rng.integers(0, 4))
     spec = synth.AttnSpec(batch, B, k, ("fixed", 0), Hkv * G, Hkv, D)
     case = synth.make_attention_case(spec, 6000 + seed, prefix_lens=P, window_lens=W, extra_pages=extra,
-                                     tail_fill=float("nan"))
+                                     tail_fill=float("nan"), v_token_major=seed % 2 == 1)
     return case, mode, split, host
 
 
@@ -47,7 +47,7 @@ def test_random_shape_parity(gpu, seed):
     case, mode, split, host = draw(seed)
     say(f"  seed {seed}: B={case.block_size} G={case.num_q_heads // case.num_kv_heads} Hkv={case.num_kv_heads} "
         f"D={case.head_dim} P={case.prefix_lens.tolist()} W={case.window_lens.tolist()} {mode} split={split} "
-        f"host={host}")
+        f"host={host} v_token_major={case.v_token_major}")
     c = case.to(DEV)
     kw = {}
     if host:
@@ -62,7 +62,7 @@ def test_random_shape_parity(gpu, seed):
     torch.cuda.synchronize()
     m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
     ref = oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
-                                  case.window_lens, case.block_size, m)
+                                  case.window_lens, case.block_size, m, v_token_major=case.v_token_major)
     assert_attn_close(out.cpu(), ref, f"seed {seed}")
 
 

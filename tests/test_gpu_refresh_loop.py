@@ -27,9 +27,9 @@ def _name(request):
     say(f"\n[gpu] {request.node.nodeid}")
 
 
-def _attn_case(seed, P, k=4, B=32, Hq=16, Hkv=4, D=128):
+def _attn_case(seed, P, k=4, B=32, Hq=16, Hkv=4, D=128, vt=False):
     spec = synth.AttnSpec(len(P), B, k, ("fixed", 0), Hq, Hkv, D)
-    return synth.make_attention_case(spec, seed, prefix_lens=P, tail_fill=float("nan"))
+    return synth.make_attention_case(spec, seed, prefix_lens=P, tail_fill=float("nan"), v_token_major=vt)
 
 
 def _attn(gpu, c, case, mode, out=None, **kw):
@@ -43,7 +43,8 @@ def _oracle(case, mode, k_pages=None, v_pages=None):
     m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
     return oracle.window_attention(case.q, case.k_pages if k_pages is None else k_pages,
                                    case.v_pages if v_pages is None else v_pages, case.page_table,
-                                   case.prefix_lens, case.window_lens, case.block_size, m)
+                                   case.prefix_lens, case.window_lens, case.block_size, m,
+                                   v_token_major=case.v_token_major)
 
 
 def _row_flags(flags, case):
@@ -110,10 +111,11 @@ def test_update_gate_and_in_place(gpu):
 @pytest.mark.parametrize("split", [0, 512])
 @pytest.mark.parametrize("mode", ["bidir", "block_causal"])
 def test_attention_block_flags(gpu, mode, split):
+    vt = split > 0                      # token-major V pages on the split runs
     """Only rows of flagged window blocks are computed and written; the
     others keep the sentinel.  Workgroups with no flagged row, with some, and
     the split-KV merge (split 512)."""
-    case = _attn_case(12, [300, 2100, 64, 1000])
+    case = _attn_case(12, [300, 2100, 64, 1000], vt=vt)
     c = case.to(DEV)
     flags = np.array([[0, 1, 0, 0], [1, 1, 1, 1], [0, 0, 0, 0], [0, 0, 1, 1]], dtype=np.uint8)
     out = torch.full_like(c.q, SENTINEL)
@@ -141,18 +143,20 @@ def test_block_diffusion_flags(gpu):
     assert_attn_close(got[keep], ref[keep], "block diffusion with flags")
 
 
-def _kv_setup(seed, D=128, Hkv=4):
+def _kv_setup(seed, D=128, Hkv=4, vt=False):
     rng = np.random.default_rng(seed)
     batch, npages, maxp = 4, 120, 24
     K = torch.from_numpy(rng.normal(size=(npages, Hkv, 16, D)).astype(np.float32)).to(torch.bfloat16)
-    V = torch.from_numpy(rng.normal(size=(npages, Hkv, D, 16)).astype(np.float32)).to(torch.bfloat16)
+    vshape = (npages, Hkv, 16, D) if vt else (npages, Hkv, D, 16)
+    V = torch.from_numpy(rng.normal(size=vshape).astype(np.float32)).to(torch.bfloat16)
     pt = rng.permutation(npages)[: batch * maxp].reshape(batch, maxp).astype(np.int32)
     return rng, K, V, pt
 
 
+@pytest.mark.parametrize("vt", [False, True], ids=["v_minor", "v_major"])
 @pytest.mark.parametrize("D", [128, 64])
-def test_kv_write_block_flags(gpu, D):
-    rng, K, V, pt = _kv_setup(D, D=D)
+def test_kv_write_block_flags(gpu, D, vt):
+    rng, K, V, pt = _kv_setup(D, D=D, vt=vt)
     start = np.array([0, 5, 100, 37], dtype=np.int32)       # aligned, mid-page, later, unaligned
     lens = np.array([128, 96, 128, 64], dtype=np.int32)
     B = 32
@@ -166,7 +170,7 @@ def test_kv_write_block_flags(gpu, D):
                  block_flags=torch.from_numpy(flags).to(DEV), block_size=B)
     torch.cuda.synchronize()
     rk, rv = oracle.kv_write(K.view(torch.int16), V.view(torch.int16), pt, start, lens, kn.view(torch.int16),
-                             vn.view(torch.int16), block_flags=flags, block_size=B)
+                             vn.view(torch.int16), block_flags=flags, block_size=B, v_token_major=vt)
     assert np.array_equal(Kd.cpu().view(torch.int16).numpy(), rk)
     assert np.array_equal(Vd.cpu().view(torch.int16).numpy(), rv)
 
@@ -189,12 +193,12 @@ def test_kv_write_skips_out_of_range_tokens(gpu):
     lib = gpu.load()
     import ctypes
     st = lib.mbe_kv_write(ctypes.c_void_p(Kd.data_ptr()), ctypes.c_void_p(Vd.data_ptr()), K.shape[0], K.shape[1],
-                          128, None, 6, None, None, 4, 32, total, None, None, None, 0, None)
+                          128, 0, None, 6, None, None, 4, 32, total, None, None, None, 0, None)
     assert st == 1                                         # NULL arguments are rejected on the host
     ptd, sd, ld = torch.from_numpy(pt).to(DEV), torch.from_numpy(start).to(DEV), torch.from_numpy(lens).to(DEV)
     knd, vnd = kn.to(DEV), vn.to(DEV)
     st = lib.mbe_kv_write(ctypes.c_void_p(Kd.data_ptr()), ctypes.c_void_p(Vd.data_ptr()), K.shape[0], K.shape[1],
-                          128, ctypes.c_void_p(ptd.data_ptr()), 6, ctypes.c_void_p(sd.data_ptr()),
+                          128, 0, ctypes.c_void_p(ptd.data_ptr()), 6, ctypes.c_void_p(sd.data_ptr()),
                           ctypes.c_void_p(ld.data_ptr()), 4, 32, total, ctypes.c_void_p(knd.data_ptr()),
                           ctypes.c_void_p(vnd.data_ptr()), None, 0,
                           ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
@@ -228,14 +232,15 @@ def _chain_logits(rng, rows, V, change, B):
     return torch.from_numpy(L).to(torch.bfloat16), torch.from_numpy(cur)
 
 
+@pytest.mark.parametrize("vt", [False, True], ids=["v_minor", "v_major"])
 @pytest.mark.parametrize("mode", ["changed", "changed_and_later"])
-def test_refresh_chain(gpu, mode):
+def test_refresh_chain(gpu, mode, vt):
     """threshold update -> block flags -> refresh set -> block-causal
     attention of the flagged blocks -> K/V write-back of those blocks -> next
     window attention, all on the device with no host read in between, against
     the same chain through the oracle."""
     B, k = 32, 4
-    case = _attn_case(21, [900, 2000, 333, 64], k=k, B=B)
+    case = _attn_case(21, [900, 2000, 333, 64], k=k, B=B, vt=vt)
     batch, W = case.batch, k * B
     rng = np.random.default_rng(22)
     change = [0 * k + 1, 2 * k + 0, 2 * k + 3, 3 * k + 2]          # (sequence, block) -> flat block ids
@@ -274,7 +279,7 @@ def test_refresh_chain(gpu, mode):
     assert_attn_close(got_r[torch.from_numpy(rf)], ref_r[rf], f"refresh attention ({mode})")
     rk, rv = oracle.kv_write(case.k_pages.view(torch.int16), case.v_pages.view(torch.int16), case.page_table,
                              case.prefix_lens, case.window_lens, kn.view(torch.int16), vn.view(torch.int16),
-                             block_flags=ref_f, block_size=B)
+                             block_flags=ref_f, block_size=B, v_token_major=vt)
     assert np.array_equal(c.k_pages.cpu().view(torch.int16).numpy(), rk)
     assert np.array_equal(c.v_pages.cpu().view(torch.int16).numpy(), rv)
     case2 = synth.AttnCase(q=q2, k_pages=torch.from_numpy(rk).view(torch.bfloat16),

@@ -47,6 +47,8 @@ ATTN_MUTATIONS = {
     "slot order reversed in page": ("slot = t % PAGE_SIZE", "slot = PAGE_SIZE - 1 - t % PAGE_SIZE"),
     "query rows not advanced per sequence": ("row0 += W", "row0 += 0"),
     "keys and queries swapped": ("S = scale * (Qb @ K.T)", "S = scale * (K[:W] @ Qb.T)[:, :1].repeat(n_all, 1)"),
+    "token-major V read token-minor": ("V = _f64(v_pages[page, kv_head, slot, :])",
+                                       "V = _f64(v_pages[page, kv_head, :, slot % v_pages.shape[3]])"),
 }
 
 
@@ -131,8 +133,10 @@ KV_MUTATIONS = {
     "block flags ignored": ("if fl is None or fl[b, t // int(block_size)]:", "if True:"),
     "block flag of the absolute position": ("fl[b, t // int(block_size)]",
                                             "fl[b, min((int(st[b]) + t) // int(block_size), fl.shape[1] - 1)]"),
-    "rows counted only when written": ("                V[page, :, :, slot] = vn[row]\n            row += 1",
-                                       "                V[page, :, :, slot] = vn[row]\n                row += 1"),
+    "rows counted only when written": ("                    V[page, :, :, slot] = vn[row]\n            row += 1",
+                                       "                    V[page, :, :, slot] = vn[row]\n                row += 1"),
+    "token-major V written token-minor": ("                    V[page, :, slot, :] = vn[row]",
+                                          "                    V[page, :, :, slot] = vn[row][:, :16]"),
 }
 
 
