@@ -33,7 +33,9 @@ PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 DEFAULT_WORKLOAD = "long_context_b64_p4096to32768_k4"
 METRIC = "edit-window attention TFLOP/s (bf16) + edit-select GB/s, % of MI355X peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", f"hbm_traffic_{DEFAULT_WORKLOAD}.txt")
+def traffic_file(workload):
+    """profiles/hbm_traffic_<workload>.txt (workload tag, with _k<k> for the span sweep)."""
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.txt")
 CALIB_COPY_BYTES = 256 << 20     # the plain device copy bench.py runs once, for counter calibration
 
 
@@ -96,16 +98,17 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic_file():
-    """The traffic summary: one `key=value ...` line per kernel."""
+def read_traffic_file(workload):
+    """The traffic summary of a workload: one `key=value ...` line per kernel."""
     out = {}
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(workload)) as f:
             for line in f:
                 if line.startswith("#") or "=" not in line:
                     continue
                 kv = dict(tok.split("=", 1) for tok in line.split())
-                out[kv["kernel"]] = kv
+                out[(kv["kernel"], kv.get("variant"))] = kv
+                out.setdefault(kv["kernel"], kv)
     except OSError:
         pass
     return out
@@ -116,10 +119,9 @@ def measured_traffic(kernel, workload, variant=None):
     (profiles/hbm_traffic_<workload>.txt), if it was taken on the current
     kernel sources, this workload and (when given) this kernel instantiation;
     else None."""
-    e = read_traffic_file().get(kernel)
+    tf = read_traffic_file(workload)
+    e = tf.get((kernel, variant)) if variant is not None else tf.get(kernel)
     if not e or e.get("kernel_sha") != kernel_source_hash() or e.get("workload") != workload:
-        return None
-    if variant is not None and e.get("variant") != variant:
         return None
     out = {"read_bytes": int(float(e["read_bytes"])), "write_bytes": int(float(e["write_bytes"])),
            "bytes_per_launch": int(float(e["read_bytes"]) + float(e["write_bytes"])),
@@ -163,7 +165,7 @@ def _variant(name):
     return m.group(1).replace(" ", "") if m else None
 
 
-def summarize_pmc(dirs, workload):
+def summarize_pmc(dirs, workload, bench_cmd=""):
     """Writes the HBM traffic summary (profiles/hbm_traffic_<workload>.txt) from
     rocprofv3 --pmc runs of this script:
     FETCH_SIZE, then WRITE_SIZE, then optionally TCC_EA0_RDREQ_{32B,64B,128B}_sum
@@ -175,7 +177,7 @@ def summarize_pmc(dirs, workload):
     sizes differs from the copy's."""
     fetch_dir, write_dir = dirs[0], dirs[1]
     req_dir = dirs[2] if len(dirs) > 2 else None
-    cmd = "python3 -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-next --no-others"
+    cmd = bench_cmd or "python3 -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-next --no-others"
     lines = ["# HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE (KiB per dispatch),",
              "# each scaled by the same counter's reading for a plain 256 MiB device copy;",
              "# req_read_bytes = 32*RDREQ_32B + 64*RDREQ_64B + 128*RDREQ_128B (TCC to memory read requests).",
@@ -188,7 +190,6 @@ def summarize_pmc(dirs, workload):
              f"-d {req_dir} -o run --output-format csv -- {cmd}"]
     scale = {}
     per_kernel = {}
-    variants = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = [r for r in _counter_rows(d) if r["Counter_Name"] == counter]
         copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
@@ -196,33 +197,34 @@ def summarize_pmc(dirs, workload):
         for r in rows:
             k = _kernel_key(r["Kernel_Name"])
             if k:
-                per_kernel.setdefault(k, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
-                variants.setdefault(k, set()).add(_variant(r["Kernel_Name"]))
+                key = (k, _variant(r["Kernel_Name"]))
+                per_kernel.setdefault(key, {}).setdefault(counter, []).append(float(r["Counter_Value"]))
     if req_dir:
         for r in _counter_rows(req_dir):
             k = _kernel_key(r["Kernel_Name"])
             if k:
-                per_kernel.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                key = (k, _variant(r["Kernel_Name"]))
+                per_kernel.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     sha = kernel_source_hash()
 
     def avg(v, c):
         x = v.get(c)
         return sum(x) / len(x) if x else None
 
-    for k, v in sorted(per_kernel.items()):
+    for (k, var), v in sorted(per_kernel.items(), key=lambda kv: (kv[0][0], kv[0][1] or "")):
         f, w = avg(v, "FETCH_SIZE"), avg(v, "WRITE_SIZE")
-        line = (f"kernel={k} workload={workload} kernel_sha={sha} fetch_kib={f:.1f} write_kib={w:.1f} "
+        if f is None or w is None:
+            continue
+        line = (f"kernel={k} variant={var} workload={workload} kernel_sha={sha} fetch_kib={f:.1f} write_kib={w:.1f} "
                 f"read_bytes={f * 1024 * scale['FETCH_SIZE']:.0f} write_bytes={w * 1024 * scale['WRITE_SIZE']:.0f} "
                 f"calibration=fetch_x{scale['FETCH_SIZE']:.3f},write_x{scale['WRITE_SIZE']:.3f}")
-        if len(variants.get(k, ())) == 1 and None not in variants[k]:
-            line += f" variant={next(iter(variants[k]))}"
         n32, n64, n128 = (avg(v, f"TCC_EA0_RDREQ_{b}_sum") for b in ("32B", "64B", "128B"))
         if n32 is not None and n64 is not None and n128 is not None:
             line += (f" rdreq_32b={n32:.0f} rdreq_64b={n64:.0f} rdreq_128b={n128:.0f} "
                      f"rdreq_all={avg(v, 'TCC_EA0_RDREQ_sum') or 0:.0f} "
                      f"req_read_bytes={32 * n32 + 64 * n64 + 128 * n128:.0f}")
         lines.append(line)
-    with open(TRAFFIC_FILE, "w") as f:
+    with open(traffic_file(workload), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -457,6 +459,59 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     }
 
 
+def _amdsmi_sample():
+    """(socket power W, [gfx clock MHz of each XCD]) from one
+    `amd-smi metric --power --clock --json`, or None."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "--power", "--clock", "--json"], capture_output=True, text=True,
+                           timeout=10)
+        g = json.loads(r.stdout)["gpu_data"][0]
+        pw = float(g["power"]["socket_power"]["value"])
+        clk = [float(v["clk"]["value"]) for k, v in g["clock"].items()
+               if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)]
+        return pw, clk
+    except Exception:
+        return None
+
+
+def sample_power(fn, seconds):
+    """Runs fn back to back for `seconds` while a host thread reads socket
+    power and the gfx clocks with amd-smi (about two readings a second); the
+    first half second, while the clocks settle, is left out.  Returns the
+    readings' summary (None fields when amd-smi gave nothing)."""
+    import threading
+    import torch
+    samples = []
+    stop = threading.Event()
+    t_start = time.perf_counter()
+
+    def poll():
+        while not stop.is_set():
+            r = _amdsmi_sample()
+            if r is not None:
+                samples.append((time.perf_counter() - t_start, r[0], r[1]))
+    th = threading.Thread(target=poll, daemon=True)
+    th.start()
+    calls = 0
+    while time.perf_counter() - t_start < seconds:
+        for _ in range(10):
+            fn()
+        calls += 10
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=15)
+    use = [x for x in samples if x[0] >= 0.5]
+    if not use:
+        return {"samples": 0, "calls": calls}
+    pw = [x[1] for x in use]
+    clk = [float(np.mean(x[2])) for x in use if x[2]]
+    return {"samples": len(use), "calls": calls, "seconds": seconds,
+            "socket_power_w": {"mean": round(float(np.mean(pw)), 1), "min": min(pw), "max": max(pw)},
+            "gfx_clock_mhz": ({"mean": round(float(np.mean(clk)), 1), "min": round(min(clk), 1),
+                               "max": round(max(clk), 1)} if clk else None)}
+
+
 def bench_pass_loop(mbe, attn_case, c, logits, edit_case, V, steps):
     """N_MBE = 5 editing passes (window attention + threshold update) of 8
     sequences x 2 blocks captured as one graph, each pass after the first
@@ -634,6 +689,10 @@ def cpu_baseline(wl, attn_case, edit_case, flops_total, edit_bytes_total, attn_s
     }
 
 
+def workload_tag(args):
+    return args.workload if args.k is None else f"{args.workload}_k{args.k}"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -649,6 +708,9 @@ def main():
     ap.add_argument("--no-next", action="store_true", help="skip timing the refresh/update/selection calls")
     ap.add_argument("--no-flush", action="store_true", help="do not flush the infinity cache before each step")
     ap.add_argument("--no-others", action="store_true", help="skip timing the other configurations")
+    ap.add_argument("--power-sample", type=float, default=0.0, metavar="SECONDS",
+                    help="after timing, run the attention and then the edit selection back to back for SECONDS each "
+                         "while amd-smi reads socket power and gfx clocks (reported under power_clock)")
     ap.add_argument("--attn-sample", type=int, default=28, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
@@ -663,17 +725,17 @@ def main():
                     help="write a markdown summary of a rocprofv3 --pmc pass of MFMA counters and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc, args.workload)
+        summarize_pmc(args.summarize_pmc, workload_tag(args), args.counter_command)
         return
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
         return
     if args.summarize_mfma:
-        summarize_mfma(*args.summarize_mfma, args.workload)
+        summarize_mfma(*args.summarize_mfma, workload_tag(args))
         return
     if args.summarize_counters:
         pmc_dir, kernel, out_md = args.summarize_counters
-        summarize_counters(pmc_dir, kernel, out_md, args.counter_command, args.workload)
+        summarize_counters(pmc_dir, kernel, out_md, args.counter_command, workload_tag(args))
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -798,7 +860,7 @@ def main():
     kernel = attention_kernel_name(attn_case, 0, vt)
     kernel_other = attention_kernel_name(attn_case, 0, not vt)
 
-    traffic = measured_traffic("window_attention", args.workload, variant=kernel)
+    traffic = measured_traffic("window_attention", workload_tag(args), variant=kernel)
     res = {
         "metric": METRIC,
         "value": round(100.0 * sol / t_step, 3),
@@ -842,11 +904,18 @@ def main():
                          "ms_min": round(float(np.min(d_edit)) * 1e3, 4), "gbs": round(edit_gbs, 1),
                          "pct_hbm_peak": round(100 * edit_gbs / PEAK_HBM_GBS, 2),
                          "algorithmic_mb": round(e_bytes / 1e6, 1),
-                         "traffic": measured_traffic("edit_select", args.workload)}
+                         "traffic": measured_traffic("edit_select", workload_tag(args))}
                         if edit_case is not None else None),
         "roofline": attention_roofline(flops, attn_bytes, t_attn, kernel, traffic),
         "wall_s": round(wall, 3),
     }
+    if args.power_sample > 0:
+        idle = _amdsmi_sample()
+        res["power_clock"] = {
+            "idle": {"socket_power_w": idle[0], "gfx_clock_mhz_mean": round(float(np.mean(idle[1])), 1)} if idle else None,
+            "attention": sample_power(attention, args.power_sample),
+            "edit_select": sample_power(edit, args.power_sample) if edit_case is not None else None,
+            "source": "amd-smi metric --power --clock --json, read by a host thread while the kernel ran back to back"}
     if edit_case is not None and not args.no_next:
         res["next_rows"] = bench_next_rows(mbe, attn_case, c, logits, cur, R, V, args.steps, edit_case)
     if not args.no_others:
