@@ -17,6 +17,7 @@ step time, with the attention TFLOP/s and edit-select GB/s alongside.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -376,6 +377,27 @@ def _time_events(fn, n):
     return ev[0].elapsed_time(ev[1]) / n / 1e3
 
 
+def _time_cold(fn, n, flush):
+    """Mean and median time of fn over n calls, each after a read of `flush`
+    (a 512 MiB buffer, so no input is served from the infinity cache), with
+    HIP events around the call alone on the current stream."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    d = []
+    for _ in range(n):
+        flush.view(torch.float32).sum()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        d.append(e0.elapsed_time(e1) / 1e3)
+    return float(np.mean(d)), float(np.median(d))
+
+
 def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     """Times the calls outside the timed step: the full threshold update with
     entropy on the step's logits (every 32 rows a block, 40% of rows masked),
@@ -389,8 +411,14 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     masked = torch.rand(R, generator=g) < 0.4
     cur_m[masked.to(dev)] = V - 1
     out = mbe.threshold_update(logits, cur_m, V - 1, B, 0.5, 0.0, with_entropy=True)
-    t_upd = _time_events(lambda: mbe.threshold_update(logits, cur_m, V - 1, B, 0.5, 0.0, with_entropy=True,
-                                                      out=out), steps)
+
+    def update():
+        mbe.threshold_update(logits, cur_m, V - 1, B, 0.5, 0.0, with_entropy=True, out=out)
+    t_upd = _time_events(update, steps)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flush.fill_(1)
+    t_upd_cold, _ = _time_cold(update, steps, flush)
+    del flush
     upd_bytes = R * V * 2 + R * (4 + 4 + 4 + 1 + 4) + R // B
     # refresh write-back of every window token (k blocks per sequence)
     P = attn_case.prefix_lens.to(dev)
@@ -451,7 +479,12 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
         "threshold_update": {"ms": round(t_upd * 1e3, 4), "rows": R, "vocab": V, "block": B,
                              "with_entropy": True, "algorithmic_mb": round(upd_bytes / 1e6, 1),
                              "gbs": round(upd_bytes / t_upd / 1e9, 1),
-                             "pct_hbm_peak": round(100 * upd_bytes / t_upd / 1e9 / PEAK_HBM_GBS, 2)},
+                             "pct_hbm_peak": round(100 * upd_bytes / t_upd / 1e9 / PEAK_HBM_GBS, 2),
+                             "timing": "back to back",
+                             "cold": {"ms": round(t_upd_cold * 1e3, 4),
+                                      "gbs": round(upd_bytes / t_upd_cold / 1e9, 1),
+                                      "pct_hbm_peak": round(100 * upd_bytes / t_upd_cold / 1e9 / PEAK_HBM_GBS, 2),
+                                      "timing": "512 MiB read before each call, as the step's edit selection"}},
         "kv_write": {"ms": round(t_kv * 1e3, 4), "tokens": T, "kv_heads": Hkv, "head_dim": D,
                      "algorithmic_mb": round(kv_bytes / 1e6, 2), "gbs": round(kv_bytes / t_kv / 1e9, 1)},
         "tail_entropy_scores": {"ms": round(t_tail * 1e3, 4), "blocks": int(scores.shape[0])},
@@ -510,6 +543,124 @@ def sample_power(fn, seconds):
             "socket_power_w": {"mean": round(float(np.mean(pw)), 1), "min": min(pw), "max": max(pw)},
             "gfx_clock_mhz": ({"mean": round(float(np.mean(clk)), 1), "min": round(min(clk), 1),
                                "max": round(max(clk), 1)} if clk else None)}
+
+
+def gemm_ceiling(n, seconds, steps):
+    """Dense bf16 GEMM ceiling of this part as a function of the operand
+    values: torch.mm (the vendor GEMM library) on n x n x n with operands
+    all zero, all one, N(0,1) x N(0,1) (the Q.K^T case) and U(0,1) x N(0,1)
+    (the P.V case), each timed with HIP events over `steps` back-to-back
+    calls and then run for `seconds` while socket power and gfx clocks are
+    read.  At the board's power limit the clock, and with it the rate,
+    depends on how much the multiplied bits toggle."""
+    import torch
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    flops = 2.0 * n ** 3
+
+    def operands(kind):
+        if kind == "zeros":
+            return (torch.zeros(n, n, dtype=torch.bfloat16, device=dev),) * 2
+        if kind == "ones":
+            return (torch.ones(n, n, dtype=torch.bfloat16, device=dev),) * 2
+        b = torch.randn(n, n, generator=g, device=dev).to(torch.bfloat16).contiguous()
+        if kind == "normal_x_normal":
+            a = torch.randn(n, n, generator=g, device=dev).to(torch.bfloat16)
+        else:
+            a = torch.rand(n, n, generator=g, device=dev).to(torch.bfloat16)
+        return a, b
+
+    res = {"shape": [n, n, n], "library": "torch.mm (bf16 in, bf16 out, fp32 accumulation)"}
+    for kind in ("zeros", "ones", "normal_x_normal", "uniform_x_normal"):
+        a, b = operands(kind)
+        c = torch.empty(n, n, dtype=torch.bfloat16, device=dev)
+
+        def mm():
+            torch.mm(a, b, out=c)
+        for _ in range(10):
+            mm()
+        torch.cuda.synchronize()
+        t = _time_events(mm, steps)
+        tf = flops / t / 1e12
+        pw = sample_power(mm, seconds) if seconds > 0 else None
+        res[kind] = {"ms": round(t * 1e3, 4), "tflops": round(tf, 1),
+                     "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2), "power_clock": pw}
+        print(f"[gemm] {kind}: {t * 1e3:.3f} ms, {tf:.0f} TFLOP/s", file=sys.stderr, flush=True)
+        del a, b, c
+    return res
+
+
+def attention_timeline(mbe, lib, names, repeats=3):
+    """Per-workgroup phase timeline of single attention calls (profiling build
+    libmbe_timeline.so).  Each workload is called after a read of 512 MiB
+    ("cold": inputs and kernel code evicted from the caches) and right after
+    another call ("warm"), one call per record.  Phases per workgroup: lengths
+    read (entry -> 1), first tile in LDS (-> 2), key loop (-> 3), epilogue
+    until its stores completed (-> 4).  The GPU is kept busy (the read, or a
+    spin after the warm-up call) while the host queues the timed call, so
+    that the events do not time the host.  `outside_us` is the HIP-event time of
+    the call minus the span from the first workgroup's start to the last
+    one's end: launch latency, the split merge kernel and the gap before it."""
+    import ctypes
+    import torch
+    import synth
+    dev = torch.device("cuda:0")
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev).fill_(1)
+    n_wg = 8192
+    res = {}
+    for name in names:
+        k, base = None, name
+        if name not in synth.WORKLOADS:
+            base, ks = name.rsplit("_k", 1)
+            k = int(ks)
+        case = synth.workload_attention(base, k_blocks=k)
+        c = case.to(dev)
+        out = torch.empty_like(c.q)
+        mp, mw = int(case.prefix_lens.max()), int(case.window_lens.max())
+
+        def call():
+            mbe.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens,
+                                 case.block_size, out=out, max_prefix_len=mp, max_window_len=mw,
+                                 host_prefix_lens=case.prefix_lens, host_window_lens=case.window_lens)
+        for _ in range(5):
+            call()
+        torch.cuda.synchronize()
+        recs = []
+        for mode in ["cold"] * repeats + ["warm"] * repeats:
+            if lib.mbe_timeline_clear() != 0:
+                raise RuntimeError("mbe_timeline_clear failed")
+            torch.cuda.synchronize()
+            if mode == "cold":
+                flush.view(torch.float32).sum()
+            else:
+                call()
+                torch.cuda._sleep(200000)       # keeps the GPU busy while the timed call is queued
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            call()
+            e1.record()
+            torch.cuda.synchronize()
+            buf = np.zeros(n_wg * 8, dtype=np.uint64)
+            if lib.mbe_timeline_read(buf.ctypes.data_as(ctypes.c_void_p), ctypes.c_size_t(buf.nbytes)) != 0:
+                raise RuntimeError("mbe_timeline_read failed")
+            t = buf.reshape(n_wg, 8).astype(np.int64)
+            t = t[t[:, 4] > 0]                      # workgroups that ran to the end
+            rel = (t[:, :5] - t[:, 0].min()) * 0.01  # 100 MHz ticks -> us
+            span = float(rel[:, 4].max())
+            ev = e0.elapsed_time(e1) * 1e3
+            ph = rel[:, 1:5] - rel[:, 0:4]
+            cyc = (t[:, 7] - t[:, 6]) / ((t[:, 4] - t[:, 0]) * 10.0)   # shader cycles per ns
+            recs.append({"mode": mode, "event_us": round(ev, 2), "workgroups": int(t.shape[0]),
+                         "start_spread_us": round(float(rel[:, 0].max()), 2),
+                         "phase_mean_us": [round(float(x), 2) for x in ph.mean(axis=0)],
+                         "phase_max_us": [round(float(x), 2) for x in ph.max(axis=0)],
+                         "span_us": round(span, 2), "outside_us": round(ev - span, 2),
+                         "clock_ghz": round(float(np.mean(cyc)), 3)})
+            print(f"[timeline] {name} {mode}: {json.dumps(recs[-1])}", file=sys.stderr, flush=True)
+        res[name] = recs
+        del c, out
+    return res
 
 
 def bench_pass_loop(mbe, attn_case, c, logits, edit_case, V, steps):
@@ -571,24 +722,11 @@ def bench_other_workloads(mbe, headline, steps):
     import torch
     import synth
     dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream(dev)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     flush.fill_(1)
 
     def timed(fn):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        d = []
-        for _ in range(steps):
-            flush.view(torch.float32).sum()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            d.append(e0.elapsed_time(e1) / 1e3)
-        return float(np.mean(d)), float(np.median(d))
+        return _time_cold(fn, steps, flush)
 
     res = {}
     for name, wl in synth.WORKLOADS.items():
@@ -632,6 +770,13 @@ def bench_other_workloads(mbe, headline, steps):
             res[tag] = r
             print(f"[bench] {tag}: attention {r['attention']['ms']:.4f} ms (token-major V "
                   f"{r['attention_v_token_major']['ms']:.4f} ms)", file=sys.stderr, flush=True)
+    # the floor under any call: one and two back-to-back launches of a
+    # one-element fill, timed the same way
+    tiny = torch.zeros(1, dtype=torch.int32, device=dev)
+    t1, _ = timed(lambda: tiny.fill_(1))
+    t2, _ = timed(lambda: (tiny.fill_(1), tiny.fill_(2)))
+    res["launch_floor"] = {"one_kernel_us": round(t1 * 1e6, 2), "two_kernels_us": round(t2 * 1e6, 2),
+                           "what": "one-element torch fill_ (one or two launches), 512 MiB read before each"}
     del flush
     return res
 
@@ -711,6 +856,12 @@ def main():
     ap.add_argument("--power-sample", type=float, default=0.0, metavar="SECONDS",
                     help="after timing, run the attention and then the edit selection back to back for SECONDS each "
                          "while amd-smi reads socket power and gfx clocks (reported under power_clock)")
+    ap.add_argument("--gemm-ceiling", type=int, default=0, metavar="N",
+                    help="only measure the bf16 GEMM ceiling (N x N x N) for several operand distributions "
+                         "(with --power-sample seconds of power and clock readings each) and exit")
+    ap.add_argument("--timeline", nargs="+", metavar="WORKLOAD",
+                    help="only record the attention's per-workgroup phase timeline on these workloads "
+                         "(span sweep as <name>_k<k>) with the profiling build libmbe_timeline.so, and exit")
     ap.add_argument("--attn-sample", type=int, default=28, help="sequences the CPU oracle times")
     ap.add_argument("--edit-sample", type=int, default=8192, help="edit rows the CPU oracle times")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="PMC_DIR",
@@ -751,9 +902,20 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    mbe.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.gemm_ceiling:
+        res = gemm_ceiling(args.gemm_ceiling, args.power_sample, max(args.steps, 20))
+        print(json.dumps({"gemm_ceiling": res}), flush=True)
+        return
+    if args.timeline:
+        from paper_2607_22663_amd.build import TIMELINE_LIB
+        lib = mbe.load(TIMELINE_LIB)
+        lib.mbe_timeline_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t]
+        lib.mbe_timeline_clear.argtypes = []
+        print(json.dumps({"attention_timeline": attention_timeline(mbe, lib, args.timeline)}), flush=True)
+        return
+    mbe.load()
 
     wl = synth.WORKLOADS[args.workload]
     print(f"[bench] generating {args.workload} (seed {wl.seed})", file=sys.stderr, flush=True)

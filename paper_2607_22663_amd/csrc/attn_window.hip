@@ -184,6 +184,13 @@ __device__ __forceinline__ uint32_t vt_load_offset() {
 // one page, so its address is a scalar page base plus a loop-invariant lane
 // offset (the empty asm statements keep the two apart, which selects the
 // scalar-base form of the load instead of 64-bit vector address arithmetic).
+// Cache policy of the K/V loads: nontemporal (the `nt` bit).  A tile is read
+// by the workgroups of one (sequence, KV head, split) at about the same time
+// and not again in the call, so its lines are marked for early eviction
+// rather than kept in the L2 and infinity cache; on the HBM-bound shapes
+// (one or two window blocks) this is 3-5% faster, elsewhere the same.
+constexpr int kStreamLoad = 2;
+
 template <int D, int VT>
 __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, int pid,
                                           const uint32_t (&koff)[Tile<D>::kLoads], char *buf) {
@@ -200,7 +207,7 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
     uint32_t ko;
     asm("" : "=v"(ko) : "0"(koff[j]), "s"(pid));
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + ko, (lds_void *)(kdst + j * 1024), 16,
-                                     0, 0);
+                                     0, kStreamLoad);
   }
   // token-minor V: LDS slot j*64 + lane of the page is dim (32j + lane/2),
   // half lane&1, and holds that dim's half v_half(d, lane & 1) (the swap is
@@ -214,7 +221,7 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
 #pragma unroll
   for (int j = 0; j < Tile<D>::kLoads; ++j)
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + vo,
-                                     (lds_void *)(vdst + j * 1024), 16, 0, 0);
+                                     (lds_void *)(vdst + j * 1024), 16, 0, kStreamLoad);
 }
 
 // Zeroes V entries of keys at or past `nvalid` (tile-relative) so that
@@ -243,8 +250,39 @@ __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
 // sequence and KV head): waves w and w + 2 own the same 64 rows and split the
 // keys, wave w taking the first and wave w + 2 the second 32-key block of
 // every tile; their partial results are added at the end.
+// Phase timeline (profiling builds only, compiled with -DMBE_TIMELINE): thread
+// 0 of each of the first kTimelineWgs workgroups records the 100 MHz real-time
+// counter at entry (0), once its lengths are read (1), when its first tile is
+// in LDS (2), after its key loop (3) and once its stores have completed (4),
+// and the shader-clock counter at entry (6) and end (7).  A workgroup that
+// exits early leaves its later entries as they were.  Product builds record
+// nothing.
+#ifdef MBE_TIMELINE
+constexpr int kTimelineWgs = 8192;
+__device__ unsigned long long g_timeline[kTimelineWgs * 8];
+#define MBE_TL(k, clock)                                                                     \
+  do {                                                                                       \
+    if (threadIdx.x == 0 && blockIdx.x < kTimelineWgs)                                       \
+      g_timeline[blockIdx.x * 8 + (k)] = clock;                                              \
+  } while (0)
+#define MBE_TL_REAL(k) MBE_TL(k, __builtin_amdgcn_s_memrealtime())
+#define MBE_TL_CYCLES(k) MBE_TL(k, __builtin_amdgcn_s_memtime())
+#define MBE_TL_END()                                                                         \
+  do {                                                                                       \
+    __builtin_amdgcn_s_waitcnt(0);                                                           \
+    MBE_TL_REAL(4);                                                                          \
+    MBE_TL_CYCLES(7);                                                                        \
+  } while (0)
+#else
+#define MBE_TL_REAL(k) do {} while (0)
+#define MBE_TL_CYCLES(k) do {} while (0)
+#define MBE_TL_END() do {} while (0)
+#endif
+
 template <int D, int MODE, int KS, int VT>
 __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
+  MBE_TL_REAL(0);
+  MBE_TL_CYCLES(6);
   // four K/V tile buffers (separate objects, so the compiler can tell which
   // in-flight direct loads a read depends on), three tiles in flight
   __shared__ __align__(1024) char lds0[Tile<D>::kBufBytes];
@@ -311,6 +349,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
   // no rows in this query tile, or a split past the sequence's last
   if (row0 >= M || split >= nsplit) return;
+  MBE_TL_REAL(1);
 
   // first query row of sequence b
   int cu = 0;
@@ -600,6 +639,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
         lds_barrier();
       }
       prologue();
+      if (run == 0) MBE_TL_REAL(2);
       if (run == 0) {
         f32x16 sc[2];
         qk_block(lds0, 0, sc);
@@ -642,6 +682,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
     if (!__syncthreads_or(bad)) break;
   }
+  MBE_TL_REAL(3);
 
   if constexpr (KS == 2) {
     // waves 2 and 3 hand their partial O and row sums (same reference) to
@@ -694,6 +735,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
           *reinterpret_cast<uint2 *>(orow + d0) = st;
         }
     }
+    MBE_TL_END();
     return;
   }
 
@@ -718,6 +760,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       *reinterpret_cast<float2 *>(pml) = make_float2(m_ref[qb], l_tot[qb]);
     }
   }
+  MBE_TL_END();
 }
 
 // Split-KV merge, run after the main kernel when some sequence was split (the
@@ -840,3 +883,20 @@ hipError_t launch_window_attention(const AttnParams &p, int head_dim, int mask_m
 }
 
 }  // namespace mbe
+
+#ifdef MBE_TIMELINE
+// Profiling builds only: copy out / clear the phase timeline of the last
+// attention launches (8 unsigned 64-bit entries per workgroup, the first
+// 8192 workgroups).  Return a hipError_t code.
+extern "C" int mbe_timeline_read(void *dst, size_t bytes) {
+  if (bytes > sizeof(mbe::g_timeline)) bytes = sizeof(mbe::g_timeline);
+  return static_cast<int>(hipMemcpyFromSymbol(dst, HIP_SYMBOL(mbe::g_timeline), bytes, 0, hipMemcpyDeviceToHost));
+}
+extern "C" int mbe_timeline_clear(void) {
+  void *ptr = nullptr;
+  hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(mbe::g_timeline));
+  if (e == hipSuccess) e = hipMemset(ptr, 0, sizeof(mbe::g_timeline));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  return static_cast<int>(e);
+}
+#endif
