@@ -398,6 +398,21 @@ def _time_cold(fn, n, flush):
     return float(np.mean(d)), float(np.median(d))
 
 
+def _host_issue_time(fn, n):
+    """Host time to issue one call of fn (mean over n calls queued behind a
+    GPU spin, so that the queue never waits on the GPU), synchronised after."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    torch.cuda._sleep(2_000_000)            # about a millisecond of GPU work ahead of the calls
+    t0 = time.perf_counter()
+    for _ in range(n):
+        fn()
+    t = (time.perf_counter() - t0) / n
+    torch.cuda.synchronize()
+    return t
+
+
 def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     """Times the calls outside the timed step: the full threshold update with
     entropy on the step's logits (every 32 rows a block, 40% of rows masked),
@@ -442,7 +457,8 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
     t_sel = _time_events(lambda: mbe.select_start_block(sc2, jcur, 4), steps)
     # one editing pass (attention + threshold update with entropy) at small
     # shapes, launched eagerly through the binding vs replayed from the
-    # multi-shape graph pool
+    # multi-shape graph pool: GPU time per pass (events) and host time to
+    # issue one pass
     from paper_2607_22663_amd.graphs import EditPassGraphs
     pool_rows = {}
     max_p = int(attn_case.prefix_lens.max())
@@ -470,7 +486,10 @@ def bench_next_rows(mbe, attn_case, c, logits, cur, R, V, steps, edit_case):
             mbe.threshold_update(lv, cv, V - 1, B, 0.5, 0.0, with_entropy=True, out=o_upd)
         t_e = _time_events(eager, steps)
         t_g = _time_events(lambda: pool.replay(nb, win), steps)
-        pool_rows[f"{nb}x{win}"] = {"eager_ms": round(t_e * 1e3, 4), "graph_ms": round(t_g * 1e3, 4)}
+        pool_rows[f"{nb}x{win}"] = {"eager_ms": round(t_e * 1e3, 4), "graph_ms": round(t_g * 1e3, 4),
+                                    "eager_host_us": round(_host_issue_time(eager, steps) * 1e6, 1),
+                                    "graph_host_us": round(_host_issue_time(lambda: pool.replay(nb, win), steps)
+                                                           * 1e6, 1)}
     del pool
     loop = bench_pass_loop(mbe, attn_case, c, logits, edit_case, V, steps)
     return {
