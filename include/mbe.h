@@ -166,14 +166,14 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
                                      const int32_t *page_table, const int32_t *prefix_lens,
                                      int32_t block_size, void *out, const mbe_attn_opts *opts);
 
-/* Workspace bytes the attention calls need for these shapes and options
+/* Workspace bytes mbe_window_attention needs for these shapes and options
  * (all of opts, host lengths included, since they shape the split plan): the
  * split-KV partial results.  0 means the plan needs no split and no
  * workspace.  When some sequence is split, the call runs a second, small
- * kernel that merges the partial results.
+ * kernel that merges the partial results.  The plan does not depend on the
+ * block size; the call itself checks that max_window_len is a multiple of it.
  * Returns (size_t)-1 if the arguments are invalid. */
-size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv,
-                                           const mbe_attn_opts *opts, int32_t block_size);
+size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts);
 
 /* Workspace bytes block_diffusion_attention needs for these shapes and
  * options.  Its split plan takes W_b = block_size for every sequence (and

@@ -98,8 +98,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.block_diffusion_attention.argtypes = [vp, ctypes.POINTER(PagedKV), vp, vp, i32, vp,
                                                   ctypes.POINTER(AttnOpts)]
         lib.block_diffusion_attention.restype = ctypes.c_int
-        lib.mbe_window_attention_workspace_size.argtypes = [ctypes.POINTER(PagedKV),
-                                                            ctypes.POINTER(AttnOpts), i32]
+        lib.mbe_window_attention_workspace_size.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts)]
         lib.mbe_window_attention_workspace_size.restype = sz
         lib.mbe_block_diffusion_workspace_size.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts), i32]
         lib.mbe_block_diffusion_workspace_size.restype = sz
@@ -225,7 +224,7 @@ def workspace_bytes_threshold_update(rows, vocab):
     return 0 if n == ctypes.c_size_t(-1).value else n
 
 
-def workspace_bytes_window_attention(q, k_pages, page_table, batch, block_size, *, max_prefix_len,
+def workspace_bytes_window_attention(q, k_pages, page_table, batch, *, max_prefix_len,
                                      max_window_len, mask_mode="bidir", kv_split_tokens=0):
     """Workspace bytes of a window_attention call planned from bounds only
     (no host lengths), as a captured graph replays it."""
@@ -234,7 +233,7 @@ def workspace_bytes_window_attention(q, k_pages, page_table, batch, block_size, 
     opts = AttnOpts(int(batch), q.shape[1], page_table.shape[1], q.shape[0], int(max_prefix_len), int(max_window_len),
                     MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode), 0.0,
                     int(kv_split_tokens), None, None, None, 0, None, None, None)
-    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts))
     if n == ctypes.c_size_t(-1).value:
         raise ValueError("invalid attention shapes")
     return n
@@ -334,7 +333,7 @@ def window_attention(q, k_pages, v_pages, page_table, prefix_lens, window_lens, 
                                         _ptr(window_lens), int(block_size), _ptr(out), ctypes.byref(opts))
 
     def size():
-        return lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), int(block_size))
+        return lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts))
 
     _check("mbe_window_attention", _call_with_workspace(call, size, opts, q.device, workspace))
     return out

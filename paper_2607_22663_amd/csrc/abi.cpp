@@ -640,11 +640,13 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
   return run_attention(q, paged_kv, page_table, prefix_lens, nullptr, block_size, block_size, out, opts);
 }
 
-size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts,
-                                           int32_t block_size) {
+size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts) {
+  // The split plan of a window call does not depend on the block size (only
+  // the call's check that the window bound is a multiple of it does), so the
+  // plan is made with block size 1.
   AttnPlan pl;
   if (!opts) return static_cast<size_t>(-1);
-  if (plan_attention(paged_kv, opts, block_size, opts->max_window_len, -1, &pl) != MBE_OK)
+  if (plan_attention(paged_kv, opts, 1, opts->max_window_len, -1, &pl) != MBE_OK)
     return static_cast<size_t>(-1);
   return pl.bytes;
 }

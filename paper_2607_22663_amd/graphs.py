@@ -99,8 +99,7 @@ class EditPassGraphs:
         n = batch * window
         self.window_lens[key] = torch.full((batch,), window, dtype=torch.int32, device=self.dev)
         a = workspace_bytes_window_attention(self.q[:n], self.k_pages, self.page_table[:batch], batch,
-                                             self.block_size, max_prefix_len=self.max_prefix_len,
-                                             max_window_len=window)
+                                             max_prefix_len=self.max_prefix_len, max_window_len=window)
         u = workspace_bytes_threshold_update(n, self.vocab)
         self._ws[key] = (torch.empty(max(a, 1), dtype=torch.uint8, device=self.dev),
                          torch.empty(max(u, 1), dtype=torch.uint8, device=self.dev))
@@ -168,7 +167,7 @@ class PassLoopGraph:
         self.action = torch.zeros(n, T, dtype=torch.uint8, device=dev)
         self.block_changed = torch.zeros(n, T // self.block_size, dtype=torch.uint8, device=dev)
         self.counts = torch.zeros(n, dtype=torch.int32, device=dev)
-        a = workspace_bytes_window_attention(self.q[0], k_pages, self.page_table, self.batch, self.block_size,
+        a = workspace_bytes_window_attention(self.q[0], k_pages, self.page_table, self.batch,
                                              max_prefix_len=self.max_prefix_len, max_window_len=self.window)
         u = workspace_bytes_threshold_update(T, self.vocab)
         self._ws_attn = torch.empty(max(a, 1), dtype=torch.uint8, device=dev)

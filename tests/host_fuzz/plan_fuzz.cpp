@@ -84,7 +84,7 @@ int main(int argc, char **argv) {
     o.host_prefix_lens = host ? P.data() : nullptr;
     o.host_window_lens = host ? W.data() : nullptr;
     const size_t need = bd ? mbe_block_diffusion_workspace_size(&kv, &o, B)
-                           : mbe_window_attention_workspace_size(&kv, &o, B);
+                           : mbe_window_attention_workspace_size(&kv, &o);
     CHECK(need != static_cast<size_t>(-1), "size query rejected a valid shape");
     fuzz::host_P = host ? P.data() : nullptr;
     fuzz::host_W = host ? W.data() : nullptr;

@@ -81,7 +81,7 @@ def test_attention_null_pointers_and_workspace(lib):
     assert st == 1 and "paged_kv" in lib.mbe_last_error().decode()
     # a plan that needs split-KV partials without a workspace
     opts = _opts(max_prefix_len=4096, max_pages_per_seq=300, kv_split_tokens=1024)
-    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32)
+    need = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts))
     assert need > 0
     st, msg = _attn(lib, kv, opts)
     assert st == 4 and "workspace" in msg
@@ -101,7 +101,7 @@ def test_block_diffusion_workspace_size_is_what_the_call_requires(lib):
                  host_prefix_lens=P.ctypes.data_as(ctypes.c_void_p))
     need = lib.mbe_block_diffusion_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32)
     assert 0 < need != ctypes.c_size_t(-1).value
-    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts), 32) < need
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(opts)) < need
     opts.workspace, opts.workspace_bytes = ctypes.c_void_p(256 * 1024), need - 1
     st = lib.block_diffusion_attention(ctypes.c_void_p(64), ctypes.byref(kv), ctypes.c_void_p(8),
                                        ctypes.c_void_p(8), 32, ctypes.c_void_p(128), ctypes.byref(opts))
@@ -121,13 +121,13 @@ def test_attention_empty_batch_is_ok_without_launch(lib):
 def test_workspace_sizes(lib):
     kv = _kv()
     small = _opts(max_prefix_len=64, kv_split_tokens=0)
-    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(small), 32) == 0
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(small)) == 0
     big = _opts(batch=1, total_q=64, max_prefix_len=16384, max_pages_per_seq=1100, kv_split_tokens=2048)
-    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(big), 32)
+    n = lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(big))
     splits = math.ceil((16384 + 64) / 2048)
     assert n >= splits * 64 * 16 * (128 + 2) * 4
     bad = _opts(num_q_heads=5)
-    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(bad), 32) == ctypes.c_size_t(-1).value
+    assert lib.mbe_window_attention_workspace_size(ctypes.byref(kv), ctypes.byref(bad)) == ctypes.c_size_t(-1).value
     assert lib.mbe_edit_select_workspace_size(8192, 131072) == 0
     assert lib.mbe_edit_select_workspace_size(64, 131072) > 0
     assert lib.mbe_edit_select_workspace_size(-1, 10) == ctypes.c_size_t(-1).value
@@ -292,7 +292,7 @@ int main(void) {
   kv.page_size = 16; kv.num_kv_heads = 4; kv.head_dim = 128; kv.num_pages = 10;
   o.batch = 1; o.num_q_heads = 16; o.max_pages_per_seq = 10; o.total_q = 64;
   o.max_prefix_len = 64; o.max_window_len = 64;
-  n = mbe_window_attention_workspace_size(&kv, &o, 32);
+  n = mbe_window_attention_workspace_size(&kv, &o);
   if (n != 0) return 1;
   kv.head_dim = 96;
   if (mbe_window_attention(NULL, &kv, NULL, NULL, NULL, 32, NULL, &o) != MBE_ERR_UNSUPPORTED) return 2;
