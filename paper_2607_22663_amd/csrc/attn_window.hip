@@ -178,12 +178,6 @@ __device__ __forceinline__ uint32_t vt_load_offset() {
   return static_cast<uint32_t>(row * (2 * D) + (((lane % RC) ^ v_swz<D>(row)) << 4));
 }
 
-// Issues this wave's direct HBM->LDS loads of one 64-key tile into `buf`:
-// wave wv fetches page wv of the tile, its K rows (swizzled) and its V page
-// ([D][16 keys], 8-key halves placed by v_half).  Each load reads 1 KB from
-// one page, so its address is a scalar page base plus a loop-invariant lane
-// offset (the empty asm statements keep the two apart, which selects the
-// scalar-base form of the load instead of 64-bit vector address arithmetic).
 // Cache policy of the K/V loads: nontemporal (the `nt` bit).  A tile is read
 // by the workgroups of one (sequence, KV head, split) at about the same time
 // and not again in the call, so its lines are marked for early eviction
@@ -191,9 +185,16 @@ __device__ __forceinline__ uint32_t vt_load_offset() {
 // (one or two window blocks) this is 3-5% faster, elsewhere the same.
 constexpr int kStreamLoad = 2;
 
+// Issues this wave's direct HBM->LDS loads of one 64-key tile into `buf`:
+// wave wv fetches page wv of the tile, its K rows (swizzled) and its V page
+// ([D][16 keys], 8-key halves placed by v_half; token-major: rows like K).
+// Each load reads 1 KB from one page, so its address is a scalar page base
+// plus a loop-invariant lane offset, koff[j] for K and voff for V (the empty
+// asm statements keep the two apart, which selects the scalar-base form of
+// the load instead of 64-bit vector address arithmetic).
 template <int D, int VT>
 __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, int pid,
-                                          const uint32_t (&koff)[Tile<D>::kLoads], char *buf) {
+                                          uint32_t *koff, uint32_t &voff, char *buf) {
   constexpr int PB = Tile<D>::kPageBytes;
   pid = __builtin_amdgcn_readfirstlane(pid);   // wave-uniform; lets it live in a scalar register
   const int64_t page = (static_cast<int64_t>(pid) * p.num_kv_heads + g) * PB;
@@ -204,23 +205,17 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
   char *vdst = buf + Tile<D>::kKBytes + wv * PB;
 #pragma unroll
   for (int j = 0; j < Tile<D>::kLoads; ++j) {
-    uint32_t ko;
-    asm("" : "=v"(ko) : "0"(koff[j]), "s"(pid));
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + ko, (lds_void *)(kdst + j * 1024), 16,
-                                     0, kStreamLoad);
+    asm("" : "+v"(koff[j]) : "s"(pid));
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + koff[j], (lds_void *)(kdst + j * 1024),
+                                     16, 0, kStreamLoad);
   }
   // token-minor V: LDS slot j*64 + lane of the page is dim (32j + lane/2),
   // half lane&1, and holds that dim's half v_half(d, lane & 1) (the swap is
   // its own inverse).  Token-major V: rows like K, swizzled by v_swz.
-  const int lane = threadIdx.x & 63;
-  uint32_t vo;
-  if constexpr (VT)
-    asm("" : "=v"(vo) : "0"(vt_load_offset<D>()), "s"(pid));
-  else
-    asm("" : "=v"(vo) : "0"((lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4)), "s"(pid));
+  asm("" : "+v"(voff) : "s"(pid));
 #pragma unroll
   for (int j = 0; j < Tile<D>::kLoads; ++j)
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + vo,
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + voff,
                                      (lds_void *)(vdst + j * 1024), 16, 0, kStreamLoad);
 }
 
@@ -537,8 +532,14 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // ---- key loop: tile t lives in buffer t % 4; tiles t+1..t+3 are in flight
   // while tile t is computed.  pid holds the page ids of the next tile to load.
+  // Per-lane offsets of the direct loads, live for the whole kernel: a load's
+  // address register is then never reused as the destination of an LDS read,
+  // which would make the compiler wait for every load in flight first.
   uint32_t kload_off[Tile<D>::kLoads];
   k_load_offsets<D>(kload_off);
+  uint32_t vload_off;
+  if constexpr (VT) vload_off = vt_load_offset<D>();
+  else vload_off = (lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4);
   int pid = 0;                                             // this wave's page of the next tile
   auto buf_of = [&](int t) -> char * {
     switch (t & 3) {
@@ -550,8 +551,22 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // direct loads of tile t into dst, then the page ids of tile t + 1
   auto issue = [&](int t, char *dst) {
-    load_tile<D, VT>(p, g, wv, pid, kload_off, dst);
+    load_tile<D, VT>(p, g, wv, pid, kload_off, vload_off, dst);
     pid = wave_page(p, b, kb + (t + 1) * kKeyTile, wv);
+  };
+  // The same into buffer t % 4 with the buffer named at each call.  The
+  // compiler tracks in-flight direct loads per LDS buffer only when it knows
+  // the buffer; a load into a computed one would make every later LDS read,
+  // the main loop's included, wait for all loads in flight.  (The asm
+  // comments keep the four calls from being merged into one with a computed
+  // destination.)
+  auto issue_any = [&](int t) {
+    switch (t & 3) {
+      case 0: issue(t, lds0); asm volatile("; tile loads into buffer 0"); break;
+      case 1: issue(t, lds1); asm volatile("; tile loads into buffer 1"); break;
+      case 2: issue(t, lds2); asm volatile("; tile loads into buffer 2"); break;
+      default: issue(t, lds3); asm volatile("; tile loads into buffer 3"); break;
+    }
   };
   constexpr int kLoadsPerTile = 2 * Tile<D>::kLoads;     // direct loads per thread per tile
   // waits until at most n tiles' loads of this thread are still in flight,
@@ -572,7 +587,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   auto prologue = [&]() {
     pid = pid0;
-    for (int t = 0; t < 3 && t < ntiles; ++t) issue(t, buf_of(t));
+    for (int t = 0; t < 3 && t < ntiles; ++t) issue_any(t);
     land(min(2, ntiles - 1));
     fix_tail(0);
   };
@@ -602,7 +617,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // one tile through dynamically chosen buffers (remainder, masked tiles)
   auto generic_step = [&](int t, bool masked) {
-    if (t + 3 < ntiles) issue(t + 3, buf_of(t + 3));
+    if (t + 3 < ntiles) issue_any(t + 3);
     if (masked) compute(buf_of(t), t, std::true_type{});
     else compute(buf_of(t), t, std::false_type{});
     if (t + 1 < ntiles) {
@@ -621,7 +636,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
         for (int qb = 0; qb < 2; ++qb) m_ref[qb] = kNegInf;
         prologue();
         for (int t = 0; t < ntiles; ++t) {
-          if (t + 3 < ntiles) issue(t + 3, buf_of(t + 3));
+          if (t + 3 < ntiles) issue_any(t + 3);
           const char *buf = buf_of(t);
           const int key0 = kb + t * kKeyTile;
           f32x16 s0[2], s1[2];

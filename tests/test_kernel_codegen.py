@@ -1,0 +1,67 @@
+"""Properties of the attention kernels' gfx950 code, checked on the assembly
+hipcc writes for them with the library's own flags (no GPU is used).
+
+The key loop keeps up to three tiles' direct HBM->LDS loads in flight and
+waits for the oldest with `s_waitcnt vmcnt(n)`, n > 0.  The compiler adds a
+wait for every load in flight (`vmcnt(0)`) before an LDS read when it cannot
+tell which buffer a load in flight writes, or when the read's destination
+register is a load's address register; one such wait in the unrolled main
+loop drains the prefetch on every pass.  Every instantiation's main loop
+(the block with the most MFMAs) must hold none, and no kernel may spill to
+scratch memory."""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _asm(tmp_path):
+    from paper_2607_22663_amd import build as b
+    try:
+        hipcc = b.hipcc()
+    except RuntimeError:
+        pytest.skip("needs hipcc")
+    flags = [f for f in b.HIPCC_FLAGS if f not in ("-shared", "-fPIC")]
+    out = tmp_path / "attn_window.s"
+    cmd = [hipcc, *flags, "--cuda-device-only", "-S", "-I", os.path.join(ROOT, "include"),
+           "-o", str(out), os.path.join(b.CSRC, "attn_window.hip")]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
+    return out.read_text()
+
+
+def _kernels(asm):
+    for m in re.finditer(r"^(_ZN3mbe12_GLOBAL__N_123window_attention_kernel\w+):", asm, re.M):
+        start = m.start()
+        yield m.group(1), asm[start:asm.index(".Lfunc_end", start)]
+
+
+def _blocks(body):
+    for blk in re.split(r"\n(?=\.LBB)", body):
+        ins = [l.strip() for l in blk.splitlines()[1:]
+               if l.strip() and not l.strip().startswith((";", "."))]
+        yield ins
+
+
+@pytest.mark.skipif(shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"),
+                    reason="needs hipcc")
+def test_attention_main_loops_never_drain_the_loads(tmp_path):
+    asm = _asm(tmp_path)
+    kernels = list(_kernels(asm))
+    assert len(kernels) == 16, [k for k, _ in kernels]       # D x mask mode x key split x V layout
+    for name, body in kernels:
+        blocks = list(_blocks(body))
+        main = max(blocks, key=lambda ins: sum("v_mfma" in l for l in ins))
+        n_mfma = sum("v_mfma" in l for l in main)
+        waits = [l for l in main if l.startswith("s_waitcnt") and "vmcnt" in l]
+        assert n_mfma >= 64, (name, n_mfma)
+        assert waits, f"{name}: main loop without a load wait"
+        drains = [l for l in waits if re.search(r"vmcnt\(0\)", l)]
+        assert not drains, f"{name}: main loop waits for every load in flight: {drains}"
+        assert not any(l.startswith(("scratch_", "buffer_store")) for l in main), name
+    for m in re.finditer(r"\.private_segment_fixed_size:\s+(\d+)", asm):
+        assert int(m.group(1)) == 0, "a kernel spills to scratch memory"
