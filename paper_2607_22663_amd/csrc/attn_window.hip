@@ -47,12 +47,17 @@
 // go from HBM straight into LDS (global_load_lds_dwordx4, no registers), four
 // buffers with three tiles in flight.  Wave w fetches page w of each tile:
 // each load instruction reads 1 KB of one page (a scalar page base plus a
-// fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled and a
-// V page ([D][16 keys]) with the two 8-key halves of every other group of 8
-// dims swapped, so that the MFMA operand reads are free of bank conflicts.
-// Work groups (split, sequence, KV head) are dealt round-robin to the XCDs,
-// and the query tiles sharing a key range run back to back on the same XCD
-// (shared L2).
+// fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled, a
+// token-minor V page ([D][16 keys]) with the two 8-key halves of every other
+// group of 8 dims swapped, a token-major one row by row with its own swizzle,
+// so that the MFMA operand reads are free of bank conflicts.  Work groups
+// (split, sequence, KV head) are dealt round-robin to the XCDs, and the query
+// tiles sharing a key range run back to back on the same XCD (shared L2).
+//
+// Targeted refresh and early exit (Sec. "Infrastructure Optimization", cache
+// control; the pass loop of Sec. "Training-Free MBE Decoding"): with block
+// flags only the rows of flagged window blocks are computed and written, and
+// with a device gate the whole call does nothing when the gate reads 0.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

@@ -35,6 +35,19 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(mbe.EXPORTS)
 
 
+def test_timeline_build_exports_the_abi_and_the_timeline_calls():
+    """The profiling build is the same library plus the phase-timeline
+    accessors; the product build has no timeline."""
+    from paper_2607_22663_amd.build import TIMELINE_LIB
+    if not os.path.exists(TIMELINE_LIB):
+        pytest.fail("libmbe_timeline.so is not built (python -m paper_2607_22663_amd.build --timeline)")
+    tl = ctypes.CDLL(TIMELINE_LIB)
+    for n in _declared_functions() + ["mbe_timeline_read", "mbe_timeline_clear"]:
+        assert hasattr(tl, n), n
+    product = ctypes.CDLL(mbe.LIB_PATH)
+    assert not hasattr(product, "mbe_timeline_read")
+
+
 def _kv(head_dim=128, page=16, hkv=4, pages=10, v_layout=0):
     return mbe.PagedKV(ctypes.c_void_p(16), ctypes.c_void_p(32), pages, page, hkv, head_dim, v_layout)
 
