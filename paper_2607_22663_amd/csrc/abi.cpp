@@ -497,8 +497,8 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   p.max_prefix = o->max_prefix_len;
   p.max_window = window_bound;
   p.qtiles = pl.qtiles;
-  // at most 128 rows per (sequence, KV head): two waves per 64 rows, each
-  // taking half of every key tile, instead of two waves with no rows
+  // at most 128 rows per (sequence, KV head): two waves per 32 rows, each
+  // taking half of every key tile, instead of four waves with no rows
   p.key_split = static_cast<int64_t>(pl.group) * window_bound <= mbe::kRowsPerTile / 2 ? 2 : 1;
   p.v_token_major = kv->v_layout == MBE_V_TOKEN_MAJOR;
   p.splits = pl.splits;

@@ -9,9 +9,10 @@
 // Work decomposition
 //   All G = Hq/Hkv query heads of a KV head share its keys, so the rows of
 //   one (sequence b, KV head g) are packed: row r = i*G + hl is window
-//   position i of query head g*G + hl.  A workgroup (4 waves, one per SIMD)
-//   owns 256 such rows and one split of the key range; a wave owns 64 rows
-//   as two 32-row MFMA column blocks.
+//   position i of query head g*G + hl.  A workgroup owns 256 such rows and
+//   one split of the key range; its 8 waves (two per
+//   SIMD, so that one wave's LDS reads and waits overlap the other's work)
+//   own 32 rows each, one 32-row MFMA column block.
 //
 // Contractions on bf16 MFMA (v_mfma_f32_32x32x16_bf16)
 //   S^T = K . Q^T : A = 32 keys x 16 dims from LDS, B = Q^T from registers.
@@ -45,9 +46,9 @@
 //
 // K/V tiles of 64 keys (four 16-token pages gathered through the page table)
 // go from HBM straight into LDS (global_load_lds_dwordx4, no registers), four
-// buffers with three tiles in flight.  Wave w fetches page w of each tile:
-// each load instruction reads 1 KB of one page (a scalar page base plus a
-// fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled, a
+// buffers with three tiles in flight.  Waves w and w + 4 fetch page w % 4 of
+// each tile, half of it each: each load instruction reads 1 KB of one page
+// (a scalar page base plus a fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled, a
 // token-minor V page ([D][16 keys]) with the two 8-key halves of every other
 // group of 8 dims swapped, a token-major one row by row with its own swizzle,
 // so that the MFMA operand reads are free of bank conflicts.  Work groups
@@ -77,6 +78,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kT = kWaves * 64;
+constexpr int QB = kRowsPerWave / 32;   // 32-row query blocks (MFMA columns) per wave
+constexpr int kPageWaves = kWaves / 4;  // waves that share the direct loads of one page
 constexpr float kNegInf = -INFINITY;
 constexpr float kSumLimit = 0x1p64f;   // row sums above this trigger the exact rerun
 constexpr bf16x2 kOnes2 = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
@@ -88,8 +91,10 @@ struct Tile {
   static constexpr int kKBytes = kKeyTile * D * 2;           // K: 64 keys x D, row-major, swizzled
   static constexpr int kVBytes = D * kKeyTile * 2;           // V: 4 pages of [D][16 keys]
   static constexpr int kBufBytes = kKBytes + kVBytes;
-  static constexpr int kLoads = kPageBytes / 1024;           // 1 KB direct loads per page (per wave, K and V each)
-  static_assert(kLoads * kWaves * 1024 == kKBytes, "one page per wave");
+  static constexpr int kLoads = kPageBytes / 1024;           // 1 KB direct loads per page, K and V each
+  static constexpr int kWaveLoads = kLoads / kPageWaves;     // of those, per wave
+  static_assert(kLoads * 4 * 1024 == kKBytes, "four pages per tile");
+  static_assert(kWaveLoads * kPageWaves == kLoads, "the waves of a page share its loads evenly");
 };
 
 // LDS chunk position of global chunk j of K row r (XOR swizzle; an involution).
@@ -146,7 +151,7 @@ __device__ __forceinline__ bf16x4 lds_read_tr4(const char *at) {
 
 typedef const __attribute__((address_space(4))) int32_t const_i32;
 
-// Page id of page `wv` of the 64-key tile starting at key0, read with a scalar
+// Page id of page `wv` (0..3) of the 64-key tile starting at key0, read with a scalar
 // load (the page table is constant during the kernel).  Slots past the table
 // row are clamped into it and ids into the pool; such pages only feed keys
 // that are masked and whose V rows are zeroed.
@@ -157,24 +162,25 @@ __device__ __forceinline__ int wave_page(const AttnParams &p, int b, int key0, i
 }
 
 // Per-lane byte offsets, within one K page, of the chunks that the direct
-// loads j = 0 .. kLoads-1 of a wave fetch: LDS slot s = 64 (kLoads wv + j) +
-// lane of the tile holds chunk (s % RC) ^ k_swz(row) of key row s / RC, and
-// row s / RC lies in page wv.  They do not depend on the tile.
+// loads j = 0 .. kWaveLoads-1 of part `part` of a page fetch (part p takes
+// the page's loads p * kWaveLoads ..): page load i fills LDS slots
+// 64 i + lane of the page, slot s holding chunk (s % RC) ^ k_swz(row) of key
+// row s / RC.  They do not depend on the tile.
 template <int D>
-__device__ __forceinline__ void k_load_offsets(uint32_t (&koff)[Tile<D>::kLoads]) {
+__device__ __forceinline__ void k_load_offsets(uint32_t (&koff)[Tile<D>::kWaveLoads], int part) {
   constexpr int RC = Tile<D>::kRowChunks;
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int j = 0; j < Tile<D>::kLoads; ++j) {
-    const int row = (j * 64 + lane) / RC;             // key within the page
+  for (int j = 0; j < Tile<D>::kWaveLoads; ++j) {
+    const int row = ((part * Tile<D>::kWaveLoads + j) * 64 + lane) / RC;   // key within the page
     const int chunk = (lane % RC) ^ k_swz<D>(row);
     koff[j] = static_cast<uint32_t>(row * (2 * D) + chunk * 16);
   }
 }
 
 // The same for a token-major V page: v_swz depends only on the row's low bits
-// (2 for D = 128, 3 for D = 64), which a lane keeps in every load j, so load j
-// reads lane offset + j KB.
+// (2 for D = 128, 3 for D = 64), which a lane keeps in every load, so page
+// load i reads lane offset + i KB.
 template <int D>
 __device__ __forceinline__ uint32_t vt_load_offset() {
   constexpr int RC = Tile<D>::kRowChunks;
@@ -191,14 +197,15 @@ __device__ __forceinline__ uint32_t vt_load_offset() {
 constexpr int kStreamLoad = 2;
 
 // Issues this wave's direct HBM->LDS loads of one 64-key tile into `buf`:
-// wave wv fetches page wv of the tile, its K rows (swizzled) and its V page
-// ([D][16 keys], 8-key halves placed by v_half; token-major: rows like K).
-// Each load reads 1 KB from one page, so its address is a scalar page base
-// plus a loop-invariant lane offset, koff[j] for K and voff for V (the empty
-// asm statements keep the two apart, which selects the scalar-base form of
-// the load instead of 64-bit vector address arithmetic).
+// waves w and w + 4 fetch page w % 4 of the tile, each one part (half) of its
+// K rows (swizzled) and of its V page ([D][16 keys], 8-key halves placed by
+// v_half; token-major: rows like K).  Each load reads 1 KB from one page, so
+// its address is a scalar page base plus a loop-invariant lane offset,
+// koff[j] for K and voff for V (the empty asm statements keep the two apart,
+// which selects the scalar-base form of the load instead of 64-bit vector
+// address arithmetic).
 template <int D, int VT>
-__device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, int pid,
+__device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wpage, int part, int pid,
                                           uint32_t *koff, uint32_t &voff, char *buf) {
   constexpr int PB = Tile<D>::kPageBytes;
   pid = __builtin_amdgcn_readfirstlane(pid);   // wave-uniform; lets it live in a scalar register
@@ -206,21 +213,22 @@ __device__ __forceinline__ void load_tile(const AttnParams &p, int g, int wv, in
   uint64_t kbase = reinterpret_cast<uint64_t>(p.k_pages) + page;
   uint64_t vbase = reinterpret_cast<uint64_t>(p.v_pages) + page;
   asm("" : "+s"(kbase), "+s"(vbase));
-  char *kdst = buf + wv * PB;
-  char *vdst = buf + Tile<D>::kKBytes + wv * PB;
+  constexpr int WL = Tile<D>::kWaveLoads;
+  char *kdst = buf + wpage * PB + part * WL * 1024;
+  char *vdst = buf + Tile<D>::kKBytes + wpage * PB + part * WL * 1024;
 #pragma unroll
-  for (int j = 0; j < Tile<D>::kLoads; ++j) {
+  for (int j = 0; j < WL; ++j) {
     asm("" : "+v"(koff[j]) : "s"(pid));
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kbase) + koff[j], (lds_void *)(kdst + j * 1024),
                                      16, 0, kStreamLoad);
   }
-  // token-minor V: LDS slot j*64 + lane of the page is dim (32j + lane/2),
+  // token-minor V: LDS slot i*64 + lane of the page is dim (32i + lane/2),
   // half lane&1, and holds that dim's half v_half(d, lane & 1) (the swap is
   // its own inverse).  Token-major V: rows like K, swizzled by v_swz.
   asm("" : "+v"(voff) : "s"(pid));
 #pragma unroll
-  for (int j = 0; j < Tile<D>::kLoads; ++j)
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + j * 1024) + voff,
+  for (int j = 0; j < WL; ++j)
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vbase + (part * WL + j) * 1024) + voff,
                                      (lds_void *)(vdst + j * 1024), 16, 0, kStreamLoad);
 }
 
@@ -246,9 +254,9 @@ __device__ __forceinline__ void zero_v_tail(char *buf, int nvalid) {
   }
 }
 
-// KS = 1: the four waves own 64 rows each.  KS = 2 (at most 128 rows per
-// sequence and KV head): waves w and w + 2 own the same 64 rows and split the
-// keys, wave w taking the first and wave w + 2 the second 32-key block of
+// KS = 1: the eight waves own 32 rows each.  KS = 2 (at most 128 rows per
+// sequence and KV head): waves w and w + 4 own the same 32 rows and split the
+// keys, wave w taking the first and wave w + 4 the second 32-key block of
 // every tile; their partial results are added at the end.
 // Phase timeline (profiling builds only, compiled with -DMBE_TIMELINE): thread
 // 0 of each of the first kTimelineWgs workgroups records the 100 MHz real-time
@@ -326,9 +334,11 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int wave = tid >> 6;
   const int c = lane & 31;       // query column of this lane
   const int h = lane >> 5;       // which half of the 32x32 MFMA layout
-  const int wrow = KS == 2 ? (wave & 1) : wave;   // 64-row slice of this wave
-  const int kown = KS == 2 ? (wave >> 1) : 0;     // 32-key block of each tile (KS = 2)
-  const int wv = __builtin_amdgcn_readfirstlane(wave);   // wave index as a scalar
+  const int wrow = KS == 2 ? (wave % (kWaves / 2)) : wave;   // row slice of this wave
+  const int kown = KS == 2 ? (wave / (kWaves / 2)) : 0;      // 32-key block of each tile (KS = 2)
+  const int wv = __builtin_amdgcn_readfirstlane(wave);       // wave index as a scalar
+  const int wpage = wv % 4;                                  // page of each tile this wave loads
+  const int wpart = wv / 4;                                  // and which part of it
   const int kb = split * p.kv_chunk;
 
   // The reads below depend only on b and are issued together: the lengths
@@ -338,7 +348,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const bool fixed = p.fixed_window >= 0;
   const int32_t P_dev = p.prefix_lens[b];
   const int32_t W_dev = (fixed ? p.prefix_lens : p.window_lens)[b];
-  const int pid0 = wave_page(p, b, kb, wv);
+  const int pid0 = wave_page(p, b, kb, wpage);
   // lengths are clamped to the host-validated bounds, so a wrong device value
   // can give wrong numbers but never an access outside q, out or the workspace
   const int W = fixed ? p.fixed_window : min(max(W_dev, 0), p.max_window);
@@ -359,40 +369,49 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     for (int j = lane; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
+    cu = __builtin_amdgcn_readfirstlane(cu);   // the same in every lane
   }
 
   // ---- this lane's two query rows (one per 32-row block of the wave), and
   // their Q^T operands in registers: lane (c, h) holds dims 16kk + 8h .. +7
-  bool valid[2];
-  int64_t qoff[2];
+  bool valid[QB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const int r = row0 + wrow * kRowsPerWave + qb * 32 + c;
     valid[qb] = r < M && cu + r / G < p.total_q &&
                 (!p.block_flags || p.block_flags[static_cast<int64_t>(b) * p.flag_stride + (r / G) / p.block_size]);
+  }
+  // index (cu + i) * Hq + hq of the output row of query block qb (row 0 for
+  // an invalid lane); recomputed where needed rather than kept over the key
+  // loop
+  auto row_index = [&](int qb) -> int64_t {
+    const int r = row0 + wrow * kRowsPerWave + qb * 32 + c;
     const int i = valid[qb] ? r / G : 0;
     const int hq = g * G + (valid[qb] ? r % G : 0);
-    qoff[qb] = (static_cast<int64_t>(cu + i) * p.num_q_heads + hq) * D;
-  }
+    return static_cast<int64_t>(cu + i) * p.num_q_heads + hq;
+  };
   // with block flags, a workgroup none of whose rows is flagged does nothing
-  if (p.block_flags && !__syncthreads_or(valid[0] || valid[1])) return;
-  constexpr int KK = D / 16;
-  bf16x8 qreg[2][KK];
+  bool any_valid = false;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
+  for (int qb = 0; qb < QB; ++qb) any_valid |= valid[qb];
+  if (p.block_flags && !__syncthreads_or(any_valid)) return;
+  constexpr int KK = D / 16;
+  bf16x8 qreg[QB][KK];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       if (valid[qb])
-        qreg[qb][kk] = *reinterpret_cast<const bf16x8 *>(p.q + qoff[qb] + kk * 16 + h * 8);
+        qreg[qb][kk] = *reinterpret_cast<const bf16x8 *>(p.q + row_index(qb) * D + kk * 16 + h * 8);
       else
         qreg[qb][kk] = bf16x8{};
     }
 
   // ---- key range of this split
   const int ke = min(n_all, kb + p.kv_chunk);
-  int lim[2];
+  int lim[QB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     int n = n_all;
     if (MODE == 1) {
       const int i = (row0 + wrow * kRowsPerWave + qb * 32 + c) / G;   // window position of the row
@@ -435,9 +454,14 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   }
 
-  f32x16 acc_o[2][DB];
-  float m_ref[2] = {kNegInf, kNegInf};   // reference, log2 units
-  float l_run[2] = {0.f, 0.f};
+  f32x16 acc_o[QB][DB];
+  float m_ref[QB];                       // reference, log2 units
+  float l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m_ref[qb] = kNegInf;
+    l_run[qb] = 0.f;
+  }
 
   // rows of this workgroup see keys [kb, lim); lim is smallest for the first
   // row, so tiles ending at or below it need no mask for any row
@@ -467,33 +491,33 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       }
   };
   // S^T of one 32-key block for both query blocks
-  auto qk_mfma = [&](const bf16x8 (&a)[KK], f32x16 (&sc)[2]) {
-    sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[0][0], f32x16{}, 0, 0, 0);
-    sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[1][0], f32x16{}, 0, 0, 0);
+  auto qk_mfma = [&](const bf16x8 (&a)[KK], f32x16 (&sc)[QB]) {
 #pragma unroll
-    for (int kk = 1; kk < KK; ++kk) {
-      sc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[0][kk], sc[0], 0, 0, 0);
-      sc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[1][kk], sc[1], 0, 0, 0);
-    }
+    for (int qb = 0; qb < QB; ++qb) sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qreg[qb][0], f32x16{}, 0, 0, 0);
+#pragma unroll
+    for (int kk = 1; kk < KK; ++kk)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+        sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qreg[qb][kk], sc[qb], 0, 0, 0);
   };
-  auto qk_block = [&](const char *buf, int kbk, f32x16 (&sc)[2]) {
+  auto qk_block = [&](const char *buf, int kbk, f32x16 (&sc)[QB]) {
     bf16x8 a[KK];
     read_k(buf, kbk, a);
     qk_mfma(a, sc);
   };
   // keys at or past a row's limit get -inf
-  auto mask_block = [&](int kblk0, f32x16 (&sc)[2]) {
+  auto mask_block = [&](int kblk0, f32x16 (&sc)[QB]) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int key = kblk0 + 16 * (v >> 3) + 8 * h + (v & 7);
         if (key >= lim[qb]) sc[qb][v] = kNegInf;
       }
   };
-  auto max_block = [&](f32x16 (&sc)[2]) {
+  auto max_block = [&](f32x16 (&sc)[QB]) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       float mx = kNegInf;
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sc[qb][v]);
@@ -502,10 +526,10 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   };
   // numerators 2^(s*scale*log2e - ref) to bf16 P^T, then O^T += V^T . P^T
-  auto softmax_pv = [&](const bf16x8 (&va)[2][DB], f32x16 (&sc)[2]) {
-    bf16x8 pb[2][2];    // [qb][m]: keys 16m + 8h .. +7 of this block
+  auto softmax_pv = [&](const bf16x8 (&va)[2][DB], f32x16 (&sc)[QB]) {
+    bf16x8 pb[QB][2];   // [qb][m]: keys 16m + 8h .. +7 of this block
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       const float msafe = (m_ref[qb] == kNegInf) ? 0.f : m_ref[qb];
       float e[16];
 #pragma unroll
@@ -531,8 +555,9 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        acc_o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[0][mm], acc_o[0][db], 0, 0, 0);
-        acc_o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[1][mm], acc_o[1][db], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          acc_o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[qb][mm], acc_o[qb][db], 0, 0, 0);
       }
   };
   // ---- key loop: tile t lives in buffer t % 4; tiles t+1..t+3 are in flight
@@ -540,8 +565,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // Per-lane offsets of the direct loads, live for the whole kernel: a load's
   // address register is then never reused as the destination of an LDS read,
   // which would make the compiler wait for every load in flight first.
-  uint32_t kload_off[Tile<D>::kLoads];
-  k_load_offsets<D>(kload_off);
+  uint32_t kload_off[Tile<D>::kWaveLoads];
+  k_load_offsets<D>(kload_off, wpart);
   uint32_t vload_off;
   if constexpr (VT) vload_off = vt_load_offset<D>();
   else vload_off = (lane >> 1) * 32 + (v_half(lane >> 1, lane & 1) << 4);
@@ -556,8 +581,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   };
   // direct loads of tile t into dst, then the page ids of tile t + 1
   auto issue = [&](int t, char *dst) {
-    load_tile<D, VT>(p, g, wv, pid, kload_off, vload_off, dst);
-    pid = wave_page(p, b, kb + (t + 1) * kKeyTile, wv);
+    load_tile<D, VT>(p, g, wpage, wpart, pid, kload_off, vload_off, dst);
+    pid = wave_page(p, b, kb + (t + 1) * kKeyTile, wpage);
   };
   // The same into buffer t % 4 with the buffer named at each call.  The
   // compiler tracks in-flight direct loads per LDS buffer only when it knows
@@ -573,7 +598,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       default: issue(t, lds3); asm volatile("; tile loads into buffer 3"); break;
     }
   };
-  constexpr int kLoadsPerTile = 2 * Tile<D>::kLoads;     // direct loads per thread per tile
+  constexpr int kLoadsPerTile = 2 * Tile<D>::kWaveLoads; // direct loads per thread per tile
   // waits until at most n tiles' loads of this thread are still in flight,
   // then meets the other waves: afterwards every earlier tile is in LDS
   auto land = [&](int n) {
@@ -599,14 +624,14 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   auto compute = [&](const char *buf, int t, auto masked) {
     const int key0 = kb + t * kKeyTile;
     if constexpr (KS == 2) {
-      f32x16 s0[2];
+      f32x16 s0[QB];
       qk_block(buf, kown, s0);
       if constexpr (decltype(masked)::value) mask_block(key0 + 32 * kown, s0);
       bf16x8 va[2][DB];
       read_v(buf, kown, va);
       softmax_pv(va, s0);
     } else {
-      f32x16 s0[2], s1[2];
+      f32x16 s0[QB], s1[QB];
       qk_block(buf, 0, s0);
       qk_block(buf, 1, s1);
       if constexpr (decltype(masked)::value) {
@@ -638,13 +663,13 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     if (ntiles > 0) {
       if (run == 1) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) m_ref[qb] = kNegInf;
+        for (int qb = 0; qb < QB; ++qb) m_ref[qb] = kNegInf;
         prologue();
         for (int t = 0; t < ntiles; ++t) {
           if (t + 3 < ntiles) issue_any(t + 3);
           const char *buf = buf_of(t);
           const int key0 = kb + t * kKeyTile;
-          f32x16 s0[2], s1[2];
+          f32x16 s0[QB], s1[QB];
           qk_block(buf, 0, s0);
           qk_block(buf, 1, s1);
           mask_block(key0, s0);
@@ -661,14 +686,14 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       prologue();
       if (run == 0) MBE_TL_REAL(2);
       if (run == 0) {
-        f32x16 sc[2];
+        f32x16 sc[QB];
         qk_block(lds0, 0, sc);
         mask_block(kb, sc);
         max_block(sc);
       }
     }
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) acc_o[qb][db] = f32x16{};
       l_run[qb] = 0.f;
@@ -696,7 +721,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     if (run == 1) break;
     bool bad = false;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       const float lt = l_run[qb] + __shfl_xor(l_run[qb], 32);
       bad |= valid[qb] && !(lt <= kSumLimit);
     }
@@ -705,15 +730,18 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   MBE_TL_REAL(3);
 
   if constexpr (KS == 2) {
-    // waves 2 and 3 hand their partial O and row sums (same reference) to
-    // waves 0 and 1 through the tile buffers, which no wave reads any more:
-    // wave 2 + j writes its O to buffer j and its sums to buffer 2
-    static_assert(2 * DB * 16 * 64 * 4 <= Tile<D>::kBufBytes, "partial O fits one buffer");
-    float *xo = reinterpret_cast<float *>(wrow == 0 ? lds0 : lds1);
-    float *xl = reinterpret_cast<float *>(lds2) + wrow * 2 * 64;
+    // the waves of the second key block hand their partial O and row sums
+    // (same reference) to the waves of the first through the tile buffers,
+    // which no wave reads any more: row slice j's O goes to buffer j / 2
+    // (half j % 2), its sums to buffer 2
+    constexpr int kXoBytes = QB * DB * 16 * 64 * 4;
+    static_assert(2 * kXoBytes <= Tile<D>::kBufBytes, "two partial O fit one buffer");
+    static_assert(kWaves / 2 <= 4, "row slices fit two buffers");
+    float *xo = reinterpret_cast<float *>((wrow < 2 ? lds0 : lds1) + (wrow & 1) * kXoBytes);
+    float *xl = reinterpret_cast<float *>(lds2) + wrow * QB * 64;
     if (kown == 1) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -724,7 +752,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     lds_barrier();
     if (kown == 1) return;      // no barrier follows
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -734,16 +762,16 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   }
 
   // ---- epilogue
-  float l_tot[2];
+  float l_tot[QB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) l_tot[qb] = l_run[qb] + __shfl_xor(l_run[qb], 32);
+  for (int qb = 0; qb < QB; ++qb) l_tot[qb] = l_run[qb] + __shfl_xor(l_run[qb], 32);
 
   if (nsplit == 1) {
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       if (!valid[qb]) continue;
       const float inv = l_tot[qb] > 0.f ? 1.f / l_tot[qb] : 0.f;
-      uint16_t *orow = p.out + qoff[qb];
+      uint16_t *orow = p.out + row_index(qb) * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -762,9 +790,9 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // split-KV: write this split's partial result (merged by the merge kernel)
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     if (!valid[qb]) continue;
-    const int64_t rowidx = qoff[qb] / D;     // (cu + i) * Hq + hq
+    const int64_t rowidx = row_index(qb);
     float *po = p.part_o + (split * split_stride + rowidx) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)

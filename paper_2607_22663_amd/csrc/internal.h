@@ -13,8 +13,8 @@ namespace mbe {
 // ---------------------------------------------------------------- attention
 constexpr int kPageSize = 16;
 constexpr int kKeyTile = 64;          // keys per LDS tile (4 pages)
-constexpr int kRowsPerWave = 64;      // packed (window position, q head) rows per wave
-constexpr int kWaves = 4;
+constexpr int kRowsPerWave = 32;      // packed (window position, q head) rows per wave
+constexpr int kWaves = 8;               // two per SIMD
 constexpr int kRowsPerTile = kRowsPerWave * kWaves;   // rows per workgroup
 constexpr int kXcds = 8;              // MI355X: workgroups go round-robin over 8 XCDs
 constexpr int kMaxOrder = 1024;       // dispatch-order entries passed in the kernel arguments
