@@ -40,6 +40,22 @@ bool debug_checks() {
   return v && v[0] == '1';
 }
 
+// Key loop of the attention with token-minor V and no key split: the
+// software-pipelined loop (scores of the next 32-key block on the matrix
+// cores while this block is exponentiated, five LDS tile buffers) when a
+// work unit spans at least kPipeMinTiles 64-key tiles; below that its longer
+// start-up costs more than it saves (measured: long-context and 8-block
+// windows over 16K prefixes gain 2%, 4-block windows and shorter loops lose
+// up to 9%).  MBE_ATTN_PIPELINE=0 / 1 forces either loop (tests use it to
+// run both on every shape).
+constexpr int64_t kPipeMinTiles = 96;
+int pipeline_override() {
+  const char *v = std::getenv("MBE_ATTN_PIPELINE");
+  if (v && v[0] == '0') return 0;
+  if (v && v[0] == '1') return 1;
+  return -1;
+}
+
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -501,6 +517,12 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   // taking half of every key tile, instead of four waves with no rows
   p.key_split = static_cast<int64_t>(pl.group) * window_bound <= mbe::kRowsPerTile / 2 ? 2 : 1;
   p.v_token_major = kv->v_layout == MBE_V_TOKEN_MAJOR;
+  {
+    const int64_t unit_keys = std::min<int64_t>(pl.kv_chunk, static_cast<int64_t>(o->max_prefix_len) + window_bound);
+    const int force = pipeline_override();
+    const bool eligible = !p.v_token_major && p.key_split == 1;
+    p.pipelined = eligible && (force >= 0 ? force == 1 : (unit_keys + mbe::kKeyTile - 1) / mbe::kKeyTile >= kPipeMinTiles);
+  }
   p.splits = pl.splits;
   p.kv_chunk = pl.kv_chunk;
   p.groups = pl.groups;

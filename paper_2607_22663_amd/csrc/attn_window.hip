@@ -287,16 +287,19 @@ __device__ unsigned long long g_timeline[kTimelineWgs * 8];
 #define MBE_TL_END() do {} while (0)
 #endif
 
-template <int D, int MODE, int KS, int VT>
+template <int D, int MODE, int KS, int VT, int PIPE>
 __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
+  static_assert(!PIPE || (KS == 1 && QB == 1), "the pipelined loop holds one 32-row block per wave");
   MBE_TL_REAL(0);
   MBE_TL_CYCLES(6);
-  // four K/V tile buffers (separate objects, so the compiler can tell which
-  // in-flight direct loads a read depends on), three tiles in flight
+  // K/V tile buffers (separate objects, so the compiler can tell which
+  // in-flight direct loads a read depends on): four with three tiles in
+  // flight, or five in the pipelined loop (PIPE)
   __shared__ __align__(1024) char lds0[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds1[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds2[Tile<D>::kBufBytes];
   __shared__ __align__(1024) char lds3[Tile<D>::kBufBytes];
+  __shared__ __align__(1024) char lds4[PIPE ? Tile<D>::kBufBytes : 1024];   // the pipelined loop's fifth
 
   // ---- work unit.  Workgroup id % 8 is the XCD that runs it.  With a
   // dispatch table the host has placed every unit (groups dealt largest
@@ -332,6 +335,26 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  // Workgroup-wide OR of a per-thread flag.  With five tile buffers it goes
+  // through one word per wave at the start of the fifth (the library's own
+  // reduction would need LDS beyond the buffers); the pipelined loop, that
+  // buffer's only other user, loads into it after barriers that follow every
+  // read here.
+  auto wg_any = [&](bool v) -> bool {
+    if constexpr (!PIPE) {
+      return __syncthreads_or(v) != 0;
+    } else {
+      volatile int *slot = reinterpret_cast<volatile int *>(lds4);
+      const bool w = __builtin_amdgcn_ballot_w64(v) != 0;
+      lds_barrier();       // earlier reads of the words are done
+      if ((tid & 63) == 0) slot[wave] = w;
+      lds_barrier();
+      bool r = false;
+#pragma unroll
+      for (int i = 0; i < kWaves; ++i) r |= slot[i] != 0;
+      return r;
+    }
+  };
   const int c = lane & 31;       // query column of this lane
   const int h = lane >> 5;       // which half of the 32x32 MFMA layout
   const int wrow = KS == 2 ? (wave % (kWaves / 2)) : wave;   // row slice of this wave
@@ -394,7 +417,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   bool any_valid = false;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) any_valid |= valid[qb];
-  if (p.block_flags && !__syncthreads_or(any_valid)) return;
+  if (p.block_flags && !wg_any(any_valid)) return;
   constexpr int KK = D / 16;
   bf16x8 qreg[QB][KK];
 #pragma unroll
@@ -470,6 +493,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int t_full = min(ntiles, max(0, (wg_min - kb) / kKeyTile));
 
   // K operands (A of S^T = K.Q^T) of 32-key block kbk
+  // (the offsets are formed at each read, from a copy of koff0 the compiler
+  // cannot see through, instead of being kept in KK registers)
   auto read_k = [&](const char *buf, int kbk, bf16x8 (&a)[KK]) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) a[kk] = lds_read8(buf, koff[kk] + kbk * 32 * (2 * D));
@@ -656,10 +681,188 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     }
   };
 
+  // ---- software-pipelined key loop (KS = 1), by 32-key block n: the
+  // scores of block n + 1 are computed on the matrix cores while block n's
+  // scores, computed one half-step earlier, are exponentiated; then block
+  // n's P.V.  Step t covers the two blocks of tile t, the second of which
+  // scores the first block of tile t + 1.  Five buffers: at the top of step t
+  // tiles t and t + 1 are in LDS and tiles t + 2, t + 3 in flight; step t
+  // issues tile t + 4 into the buffer of tile t - 1, which every wave
+  // finished reading before the barrier that ended step t - 1, and its own
+  // barrier lands tile t + 2.  Every LDS read of step t is of tile t or t + 1.
+    // numerators of one block to bf16 P^T (keys 16m + 8h .. +7), row sums of
+  // the bf16 numerators
+  auto softmax_blk = [&](const f32x16 (&s)[QB], bf16x8 (&pb)[2]) {
+    const float msafe = (m_ref[0] == kNegInf) ? 0.f : m_ref[0];
+    float e[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) e[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][v], p.scale_log2, -msafe));
+    float lsum = l_run[0];
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm) {
+      const u32x4 w = {pack_bf16x2(e[8 * mm + 0], e[8 * mm + 1]), pack_bf16x2(e[8 * mm + 2], e[8 * mm + 3]),
+                       pack_bf16x2(e[8 * mm + 4], e[8 * mm + 5]), pack_bf16x2(e[8 * mm + 6], e[8 * mm + 7])};
+      pb[mm] = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t wk = w[k];
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wk), kOnes2, lsum, false);
+      }
+    }
+    l_run[0] = lsum;
+  };
+  // O^T += V^T . P^T for one block
+  auto pv_mfma = [&](const bf16x8 (&va)[2][DB], const bf16x8 (&pb)[2]) {
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        acc_o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[mm][db], pb[mm], acc_o[0][db], 0, 0, 0);
+  };
+  // half-step for block n = block kbk of the tile in vbuf: s holds its
+  // scores on entry and those of block n + 1 (block nkbk of the tile in
+  // nbuf, first key nkey0) on exit
+  auto half_step = [&](const char *vbuf, int kbk, const char *nbuf, int nkbk, int nkey0, f32x16 (&s)[QB],
+                       auto masked) {
+    bf16x8 va[2][DB];
+    read_v(vbuf, kbk, va);
+    f32x16 sn[QB];
+    qk_block(nbuf, nkbk, sn);
+    if constexpr (decltype(masked)::value) mask_block(nkey0, sn);
+    bf16x8 pb[2];
+    softmax_blk(s, pb);
+    pv_mfma(va, pb);
+    s[0] = sn[0];
+  };
+  auto pipe_step = [&](const char *vbuf, const char *kbuf, int t, f32x16 (&s)[QB], auto masked) {
+    const int key0 = kb + t * kKeyTile;
+    half_step(vbuf, 0, vbuf, 1, key0 + 32, s, masked);
+    half_step(vbuf, 1, kbuf, 0, key0 + kKeyTile, s, masked);
+  };
+  auto pipe_last = [&](const char *vbuf, int t, f32x16 (&s)[QB]) {
+    half_step(vbuf, 0, vbuf, 1, kb + t * kKeyTile + 32, s, std::true_type{});
+    bf16x8 va[2][DB];
+    read_v(vbuf, 1, va);
+    bf16x8 pb[2];
+    softmax_blk(s, pb);
+    pv_mfma(va, pb);
+  };
+  // buffer t % 5 named at each use (see issue_any)
+  auto buf5 = [&](int t) -> char * {
+    switch (t % 5) {
+      case 0: return lds0;
+      case 1: return lds1;
+      case 2: return lds2;
+      case 3: return lds3;
+      default: return lds4;
+    }
+  };
+  auto issue5 = [&](int t) {
+    switch (t % 5) {
+      case 0: issue(t, lds0); asm volatile("; tile loads into buffer 0"); break;
+      case 1: issue(t, lds1); asm volatile("; tile loads into buffer 1"); break;
+      case 2: issue(t, lds2); asm volatile("; tile loads into buffer 2"); break;
+      case 3: issue(t, lds3); asm volatile("; tile loads into buffer 3"); break;
+      default: issue(t, lds4); asm volatile("; tile loads into buffer 4"); break;
+    }
+  };
+  auto fix_tail5 = [&](int t) {
+    const int key0 = kb + t * kKeyTile;
+    if (key0 + kKeyTile > n_all) {
+      zero_v_tail<D, VT>(buf5(t), n_all - key0);
+      lds_barrier();
+    }
+  };
+  auto pipelined_run = [&](bool set_ref) {
+    pid = pid0;
+    for (int t = 0; t < 4 && t < ntiles; ++t) issue5(t);
+    land(min(2, max(0, ntiles - 2)));    // tiles 0 and 1
+    fix_tail(0);
+    if (ntiles > 1) fix_tail(1);
+    MBE_TL_REAL(2);
+    // the first block's scores; in the first run they give the reference
+    f32x16 s[QB];
+    qk_block(lds0, 0, s);
+    if (t_full == 0) mask_block(kb, s);
+    if (set_ref) max_block(s);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc_o[0][db] = f32x16{};
+    l_run[0] = 0.f;
+    int t = 0;
+    // five steps per iteration through fixed buffers; the blocks scored here
+    // need no mask and every tile issued here exists
+    for (; t + 8 < ntiles && t + 5 < t_full; t += 5) {
+      issue(t + 4, lds4);
+      pipe_step(lds0, lds1, t, s, std::false_type{});
+      land(2);
+      issue(t + 5, lds0);
+      pipe_step(lds1, lds2, t + 1, s, std::false_type{});
+      land(2);
+      issue(t + 6, lds1);
+      pipe_step(lds2, lds3, t + 2, s, std::false_type{});
+      land(2);
+      issue(t + 7, lds2);
+      pipe_step(lds3, lds4, t + 3, s, std::false_type{});
+      land(2);
+      issue(t + 8, lds3);
+      pipe_step(lds4, lds0, t + 4, s, std::false_type{});
+      land(2);
+    }
+    for (; t < ntiles; ++t) {
+      if (t + 4 < ntiles) issue5(t + 4);
+      if (t + 1 == ntiles) pipe_last(buf5(t), t, s);
+      else if (t + 1 >= t_full) pipe_step(buf5(t), buf5(t + 1), t, s, std::true_type{});
+      else pipe_step(buf5(t), buf5(t + 1), t, s, std::false_type{});
+      if (t + 2 < ntiles) {
+        land(min(2, ntiles - 3 - t));
+        fix_tail5(t + 2);
+      }
+    }
+    lds_barrier();      // all waves done with the buffers
+  };
+
   // Run 0 takes the reference from the first 32-key block.  Run 1 happens
   // only if some row sum left the safe range: it first finds the true row
   // maxima with a K.Q-only pass, then repeats the full pass.
   for (int run = 0; run < 2; ++run) {
+    if constexpr (PIPE) {
+      if (run == 1 && ntiles > 0) {
+        // the true row maxima, from a scores-only pass
+        m_ref[0] = kNegInf;
+        prologue();
+        for (int t = 0; t < ntiles; ++t) {
+          if (t + 3 < ntiles) issue_any(t + 3);
+          const char *buf = buf_of(t);
+          const int key0 = kb + t * kKeyTile;
+          f32x16 s0[QB], s1[QB];
+          qk_block(buf, 0, s0);
+          qk_block(buf, 1, s1);
+          mask_block(key0, s0);
+          mask_block(key0 + 32, s1);
+          max_block(s0);
+          max_block(s1);
+          if (t + 1 < ntiles) {
+            land(min(2, ntiles - 2 - t));
+            fix_tail(t + 1);
+          }
+        }
+        lds_barrier();
+      }
+      if (ntiles > 0) pipelined_run(run == 0);
+      else {
+        l_run[0] = 0.f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc_o[0][db] = f32x16{};
+      }
+      if (run == 1) break;
+      bool bad = false;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const float lt = l_run[qb] + __shfl_xor(l_run[qb], 32);
+        bad |= valid[qb] && !(lt <= kSumLimit);
+      }
+      if (!wg_any(bad)) break;
+    } else {
     if (ntiles > 0) {
       if (run == 1) {
 #pragma unroll
@@ -725,19 +928,20 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
       const float lt = l_run[qb] + __shfl_xor(l_run[qb], 32);
       bad |= valid[qb] && !(lt <= kSumLimit);
     }
-    if (!__syncthreads_or(bad)) break;
+    if (!wg_any(bad)) break;
+    }
   }
   MBE_TL_REAL(3);
 
   if constexpr (KS == 2) {
     // the waves of the second key block hand their partial O and row sums
     // (same reference) to the waves of the first through the tile buffers,
-    // which no wave reads any more: row slice j's O goes to buffer j / 2
-    // (half j % 2), its sums to buffer 2
+    // which no wave reads any more: row slice j's O goes to buffer 0 or 1
+    // (as many slices per buffer as fit), its sums to buffer 2
     constexpr int kXoBytes = QB * DB * 16 * 64 * 4;
-    static_assert(2 * kXoBytes <= Tile<D>::kBufBytes, "two partial O fit one buffer");
-    static_assert(kWaves / 2 <= 4, "row slices fit two buffers");
-    float *xo = reinterpret_cast<float *>((wrow < 2 ? lds0 : lds1) + (wrow & 1) * kXoBytes);
+    constexpr int kSlicesPerBuf = Tile<D>::kBufBytes / kXoBytes;
+    static_assert(kSlicesPerBuf >= 1 && kWaves / 2 <= 2 * kSlicesPerBuf, "row slices fit two buffers");
+    float *xo = reinterpret_cast<float *>((wrow < kSlicesPerBuf ? lds0 : lds1) + (wrow % kSlicesPerBuf) * kXoBytes);
     float *xl = reinterpret_cast<float *>(lds2) + wrow * QB * 64;
     if (kown == 1) {
 #pragma unroll
@@ -909,11 +1113,12 @@ hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
   const int64_t grid = p.order_kind == kOrderUnits ? p.order_n : p.slots_per_xcd * kXcds;
   const dim3 g(static_cast<unsigned>(grid)), blk(kT);
   if (p.v_token_major) {
-    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 1>), g, blk, 0, stream, p);
-    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 1>), g, blk, 0, stream, p);
+    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 1, 0>), g, blk, 0, stream, p);
+    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 1, 0>), g, blk, 0, stream, p);
   } else {
-    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 0>), g, blk, 0, stream, p);
-    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 0>), g, blk, 0, stream, p);
+    if (p.key_split == 2) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 2, 0, 0>), g, blk, 0, stream, p);
+    else if (p.pipelined) hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 0, 1>), g, blk, 0, stream, p);
+    else hipLaunchKernelGGL((window_attention_kernel<D, MODE, 1, 0, 0>), g, blk, 0, stream, p);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits == 1) return e;

@@ -40,6 +40,7 @@ struct AttnParams {
   int32_t qtiles, splits, kv_chunk;
   int32_t key_split;          // 1, or 2 when a sequence has at most 128 rows per KV head
   int32_t v_token_major;      // V pages [16][D] (like K) instead of [D][16]
+  int32_t pipelined;          // software-pipelined key loop (token-minor V, no key split)
   int64_t groups;             // (split, sequence rank, KV head) groups of qtiles work units
   int64_t slots_per_xcd;      // grid = kXcds * slots_per_xcd workgroups
   float scale_log2;           // softmax scale * log2(e)
