@@ -56,14 +56,19 @@ def attention_work(case):
 RIDGE_FLOP_PER_BYTE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # ~315
 
 
-def attention_kernel_name(case, mode=0, v_token_major=False, max_window=None):
-    """The window_attention_kernel<D, MODE, KS, VT> instantiation a call runs:
-    KS = 2 (two waves per 64 rows, each taking half of every key tile) when a
-    sequence has at most 128 (query head, window position) rows per KV head."""
-    G = case.num_q_heads // case.num_kv_heads
-    w = int(case.window_lens.max()) if max_window is None else max_window
-    ks = 2 if G * w <= 128 else 1
-    return f"window_attention_kernel<{case.head_dim},{mode},{ks},{int(bool(v_token_major))}>"
+def attention_kernel_name(case, mode=0, v_token_major=False, kv_split_tokens=0):
+    """The window_attention_kernel<D, MODE, KS, VT, PIPE> instantiation a call
+    on this case runs (bounds and host lengths as the bench passes them), from
+    the library's own launch plan (mbe_window_attention_plan)."""
+    import paper_2607_22663_amd as mbe
+    kp = case.k_pages
+    vp = kp if v_token_major else kp.transpose(2, 3)       # only the shape is read
+    plan = mbe.window_attention_plan(case.num_q_heads, kp, vp, case.page_table, case.batch, int(case.q.shape[0]),
+                                     max_prefix_len=int(case.prefix_lens.max()),
+                                     max_window_len=int(case.window_lens.max()), mask_mode=mode,
+                                     kv_split_tokens=kv_split_tokens, host_prefix_lens=case.prefix_lens,
+                                     host_window_lens=case.window_lens)
+    return plan["kernel"]
 
 
 def attention_roofline(flops, nbytes, seconds, kernel, traffic=None):
@@ -1038,8 +1043,8 @@ def main():
             d_other.append(e0.elapsed_time(e1) / 1e3)
     del other_v, flush
     t_other = float(np.mean(d_other))
-    kernel = attention_kernel_name(attn_case, 0, vt)
-    kernel_other = attention_kernel_name(attn_case, 0, not vt)
+    kernel = attention_kernel_name(attn_case, 0, vt, args.kv_split_tokens)
+    kernel_other = attention_kernel_name(attn_case, 0, not vt, args.kv_split_tokens)
 
     traffic = measured_traffic("window_attention", workload_tag(args), variant=kernel)
     res = {

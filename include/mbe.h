@@ -175,6 +175,22 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
  * Returns (size_t)-1 if the arguments are invalid. */
 size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts);
 
+/* Launch plan of mbe_window_attention for these shapes and options, made on
+ * the host exactly as the call makes it (no device access): for profiling
+ * tools and tuning.  Not needed to run the call. */
+typedef struct {
+  int32_t splits;       /* key-range splits per sequence (1 = no split-KV merge) */
+  int32_t kv_chunk;     /* keys per split                                        */
+  int32_t key_split;    /* 2: two waves share every key tile of one row block    */
+  int32_t pipelined;    /* 1: the software-pipelined key loop                    */
+  int64_t workgroups;   /* grid size of the main kernel                          */
+} mbe_attn_plan;
+
+/* Fills *plan; returns MBE_OK, or an error status (and leaves *plan alone)
+ * when the arguments are invalid, as mbe_window_attention_workspace_size
+ * would return (size_t)-1. */
+mbe_status mbe_window_attention_plan(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts, mbe_attn_plan *plan);
+
 /* Workspace bytes block_diffusion_attention needs for these shapes and
  * options.  Its split plan takes W_b = block_size for every sequence (and
  * the host prefix lengths when given), so it can differ from

@@ -30,7 +30,7 @@ EXPORTS = ("mbe_window_attention", "block_diffusion_attention", "mbe_window_atte
            "mbe_block_diffusion_workspace_size", "mbe_edit_select", "mbe_edit_select_workspace_size",
            "mbe_threshold_update", "mbe_threshold_update_workspace_size", "mbe_tail_entropy_scores",
            "mbe_select_start_block", "mbe_kv_write", "mbe_refresh_blocks", "mbe_status_string", "mbe_last_error",
-           "mbe_threshold_update_noalloc")
+           "mbe_threshold_update_noalloc", "mbe_window_attention_plan")
 ACTIONS = {"keep": 0, "unmask": 1, "force_unmask": 2, "edit": 3}
 REFRESH_MODES = {"changed": 0, "changed_and_later": 1}
 
@@ -74,6 +74,11 @@ class AttnOpts(ctypes.Structure):
                 ("block_flags", ctypes.c_void_p), ("run_if_nonzero", ctypes.c_void_p)]
 
 
+class AttnPlan(ctypes.Structure):
+    _fields_ = [("splits", ctypes.c_int32), ("kv_chunk", ctypes.c_int32), ("key_split", ctypes.c_int32),
+                ("pipelined", ctypes.c_int32), ("workgroups", ctypes.c_int64)]
+
+
 _lib = None
 _lock = threading.Lock()
 
@@ -100,6 +105,9 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         lib.block_diffusion_attention.restype = ctypes.c_int
         lib.mbe_window_attention_workspace_size.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts)]
         lib.mbe_window_attention_workspace_size.restype = sz
+        lib.mbe_window_attention_plan.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts),
+                                                  ctypes.POINTER(AttnPlan)]
+        lib.mbe_window_attention_plan.restype = ctypes.c_int
         lib.mbe_block_diffusion_workspace_size.argtypes = [ctypes.POINTER(PagedKV), ctypes.POINTER(AttnOpts), i32]
         lib.mbe_block_diffusion_workspace_size.restype = sz
         lib.mbe_edit_select.argtypes = [vp, i64, i64, i64, vp, ctypes.c_float, vp, vp, vp, vp, sz, vp]
@@ -237,6 +245,31 @@ def workspace_bytes_window_attention(q, k_pages, page_table, batch, *, max_prefi
     if n == ctypes.c_size_t(-1).value:
         raise ValueError("invalid attention shapes")
     return n
+
+
+def window_attention_plan(num_q_heads, k_pages, v_pages, page_table, batch, total_q, *, max_prefix_len,
+                          max_window_len, mask_mode="bidir", kv_split_tokens=0, host_prefix_lens=None,
+                          host_window_lens=None):
+    """The launch plan a window_attention call with these shapes makes (host
+    only): dict of splits, kv_chunk, key_split, pipelined, workgroups, and the
+    main kernel's name as rocprofv3 reports it (window_attention_kernel<D,
+    MODE, KS, VT, PIPE>)."""
+    lib = load()
+    layout = v_layout_of(k_pages, v_pages)
+    kv = PagedKV(None, None, k_pages.shape[0], k_pages.shape[2], k_pages.shape[1], k_pages.shape[3], layout)
+    hp = _host_i32(host_prefix_lens, batch, "host_prefix_lens")
+    hw = _host_i32(host_window_lens, batch, "host_window_lens")
+    mode = MASK_MODES[mask_mode] if isinstance(mask_mode, str) else int(mask_mode)
+    opts = AttnOpts(int(batch), int(num_q_heads), page_table.shape[1], int(total_q), int(max_prefix_len),
+                    int(max_window_len), mode, 0.0, int(kv_split_tokens), _ptr(hp), _ptr(hw), None, 0, None,
+                    None, None)
+    plan = AttnPlan()
+    _check("mbe_window_attention_plan", lib.mbe_window_attention_plan(ctypes.byref(kv), ctypes.byref(opts),
+                                                                      ctypes.byref(plan)))
+    d = {f: getattr(plan, f) for f, _ in AttnPlan._fields_}
+    d["kernel"] = (f"window_attention_kernel<{k_pages.shape[3]},{mode},{plan.key_split},"
+                   f"{int(layout == V_TOKEN_MAJOR)},{plan.pipelined}>")
+    return d
 
 
 def _stream(device) -> ctypes.c_void_p:

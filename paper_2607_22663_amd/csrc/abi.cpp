@@ -461,6 +461,20 @@ mbe_status debug_check_kv_write(const int32_t *page_table, int32_t max_pages, in
   return MBE_OK;
 }
 
+// At most 128 rows per (sequence, KV head): two waves per 32 rows, each
+// taking half of every key tile, instead of four waves with no rows.
+int32_t key_split_of(const AttnPlan &pl, int32_t window_bound) {
+  return static_cast<int64_t>(pl.group) * window_bound <= mbe::kRowsPerTile / 2 ? 2 : 1;
+}
+
+bool use_pipelined(const mbe_paged_kv *kv, const mbe_attn_opts *o, const AttnPlan &pl, int32_t window_bound,
+                   int32_t key_split) {
+  const int64_t unit_keys = std::min<int64_t>(pl.kv_chunk, static_cast<int64_t>(o->max_prefix_len) + window_bound);
+  const int force = pipeline_override();
+  const bool eligible = kv->v_layout != MBE_V_TOKEN_MAJOR && key_split == 1;
+  return eligible && (force >= 0 ? force == 1 : (unit_keys + mbe::kKeyTile - 1) / mbe::kKeyTile >= kPipeMinTiles);
+}
+
 mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *page_table,
                          const int32_t *prefix_lens, const int32_t *window_lens, int32_t block_size,
                          int32_t fixed_window, void *out, const mbe_attn_opts *o) {
@@ -513,16 +527,9 @@ mbe_status run_attention(const void *q, const mbe_paged_kv *kv, const int32_t *p
   p.max_prefix = o->max_prefix_len;
   p.max_window = window_bound;
   p.qtiles = pl.qtiles;
-  // at most 128 rows per (sequence, KV head): two waves per 32 rows, each
-  // taking half of every key tile, instead of four waves with no rows
-  p.key_split = static_cast<int64_t>(pl.group) * window_bound <= mbe::kRowsPerTile / 2 ? 2 : 1;
+  p.key_split = key_split_of(pl, window_bound);
   p.v_token_major = kv->v_layout == MBE_V_TOKEN_MAJOR;
-  {
-    const int64_t unit_keys = std::min<int64_t>(pl.kv_chunk, static_cast<int64_t>(o->max_prefix_len) + window_bound);
-    const int force = pipeline_override();
-    const bool eligible = !p.v_token_major && p.key_split == 1;
-    p.pipelined = eligible && (force >= 0 ? force == 1 : (unit_keys + mbe::kKeyTile - 1) / mbe::kKeyTile >= kPipeMinTiles);
-  }
+  p.pipelined = use_pipelined(kv, o, pl, window_bound, p.key_split);
   p.splits = pl.splits;
   p.kv_chunk = pl.kv_chunk;
   p.groups = pl.groups;
@@ -660,6 +667,20 @@ mbe_status block_diffusion_attention(const void *q, const mbe_paged_kv *paged_kv
                                      const mbe_attn_opts *opts) {
   if (block_size < 1) return fail(MBE_ERR_BAD_SHAPE, "block_size %d < 1", block_size);
   return run_attention(q, paged_kv, page_table, prefix_lens, nullptr, block_size, block_size, out, opts);
+}
+
+mbe_status mbe_window_attention_plan(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts, mbe_attn_plan *plan) {
+  if (!opts || !plan) return fail(MBE_ERR_NULL_ARG, "opts and plan must not be NULL");
+  AttnPlan pl;
+  const mbe_status st = plan_attention(paged_kv, opts, 1, opts->max_window_len, -1, &pl);
+  if (st != MBE_OK) return st;
+  const int32_t ks = key_split_of(pl, opts->max_window_len);
+  plan->splits = pl.splits;
+  plan->kv_chunk = pl.kv_chunk;
+  plan->key_split = ks;
+  plan->pipelined = use_pipelined(paged_kv, opts, pl, opts->max_window_len, ks) ? 1 : 0;
+  plan->workgroups = pl.order_kind == mbe::kOrderUnits ? pl.order_n : pl.slots_per_xcd * mbe::kXcds;
+  return MBE_OK;
 }
 
 size_t mbe_window_attention_workspace_size(const mbe_paged_kv *paged_kv, const mbe_attn_opts *opts) {

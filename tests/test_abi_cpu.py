@@ -29,7 +29,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 16, names
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(mbe.EXPORTS)
@@ -377,3 +377,45 @@ def test_threshold_update_noalloc_rejects_on_the_host(lib):
     assert call(64, omega=float("nan")) == 6
     assert call(30) == 2                    # not a multiple of the block
     assert call(0) == 0                     # nothing to do
+
+
+def _plan(B=32, k=4, P=None, batch=64, Hq=16, Hkv=4, D=128, token_major=False, split=0):
+    """mbe_window_attention_plan through the binding, for shapes only (meta
+    tensors: no memory, no GPU)."""
+    P = np.asarray(P if P is not None else [32 * (128 + 14 * i) for i in range(batch)], dtype=np.int32)
+    W = np.full(batch, k * B, dtype=np.int32)
+    pages = int(sum(-(-(p + w) // 16) for p, w in zip(P, W)))
+    kp = torch.empty((pages, Hkv, 16, D), dtype=torch.bfloat16, device="meta")
+    vp = kp if token_major else torch.empty((pages, Hkv, D, 16), dtype=torch.bfloat16, device="meta")
+    pt = torch.empty((batch, int(-(-(P.max() + W.max()) // 16))), dtype=torch.int32, device="meta")
+    return mbe.window_attention_plan(Hq, kp, vp, pt, batch, int(W.sum()), max_prefix_len=int(P.max()),
+                                     max_window_len=int(W.max()), kv_split_tokens=split,
+                                     host_prefix_lens=P, host_window_lens=W)
+
+
+def test_attention_plan_picks_the_kernel_variant(lib, monkeypatch):
+    """The plan query reports the kernel the call will run: the pipelined key
+    loop for long token-minor units without key split, the key-split waves for
+    at most 128 rows per KV head, and splits exactly when a workspace is
+    needed."""
+    monkeypatch.delenv("MBE_ATTN_PIPELINE", raising=False)
+    long_ctx = _plan()                                  # 64 x P up to 32K, k = 4: no split
+    assert long_ctx["kernel"] == "window_attention_kernel<128,0,1,0,1>"
+    assert long_ctx["splits"] == 1 and long_ctx["workgroups"] >= 512
+    assert _plan(token_major=True)["kernel"] == "window_attention_kernel<128,0,1,1,0>"
+    span = dict(batch=8, P=[16384] * 8)
+    k1, k4, k8 = _plan(k=1, **span), _plan(k=4, **span), _plan(k=8, **span)
+    assert (k1["key_split"], k1["pipelined"]) == (2, 0) and k1["splits"] > 1
+    assert k4["pipelined"] == 0 and k4["kv_chunk"] // 64 < 96          # short units keep the plain loop
+    assert k8["pipelined"] == 1 and k8["kv_chunk"] // 64 >= 96
+    monkeypatch.setenv("MBE_ATTN_PIPELINE", "0")
+    assert _plan()["pipelined"] == 0
+    monkeypatch.setenv("MBE_ATTN_PIPELINE", "1")
+    assert _plan(k=4, **span)["pipelined"] == 1
+    assert _plan(k=1, **span)["pipelined"] == 0                          # key split: not eligible
+    assert _plan(token_major=True)["pipelined"] == 0                     # token-major V: not eligible
+    raw = ctypes.CDLL(mbe.LIB_PATH)             # plain pointers, whatever classes the binding holds
+    raw.mbe_window_attention_plan.argtypes = [ctypes.c_void_p] * 3
+    kv, opts, bad_opts, out = _kv(), _opts(), _opts(num_q_heads=5), ctypes.create_string_buffer(64)
+    assert raw.mbe_window_attention_plan(ctypes.addressof(kv), ctypes.addressof(opts), None) == 1
+    assert raw.mbe_window_attention_plan(ctypes.addressof(kv), ctypes.addressof(bad_opts), ctypes.addressof(out)) == 2
