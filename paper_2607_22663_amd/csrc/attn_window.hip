@@ -493,8 +493,6 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int t_full = min(ntiles, max(0, (wg_min - kb) / kKeyTile));
 
   // K operands (A of S^T = K.Q^T) of 32-key block kbk
-  // (the offsets are formed at each read, from a copy of koff0 the compiler
-  // cannot see through, instead of being kept in KK registers)
   auto read_k = [&](const char *buf, int kbk, bf16x8 (&a)[KK]) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) a[kk] = lds_read8(buf, koff[kk] + kbk * 32 * (2 * D));
