@@ -529,14 +529,28 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     qk_mfma(a, sc);
   };
   // keys at or past a row's limit get -inf
+  // Element v of a lane holds key kblk0 + 8h + 16(v >> 3) + (v & 7).  With
+  // token-major V the test is against the lane's room left, so each compare
+  // takes a constant instead of one of 16 key offsets the compiler would
+  // keep in registers (that kernel then needs no scratch; in the others the
+  // same form makes the register allocation spill more, not less).
   auto mask_block = [&](int kblk0, f32x16 (&sc)[QB]) {
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < QB; ++qb) {
+      if constexpr (VT) {
+        int room = lim[qb] - kblk0 - 8 * h;
+        asm volatile("" : "+v"(room));
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kblk0 + 16 * (v >> 3) + 8 * h + (v & 7);
-        if (key >= lim[qb]) sc[qb][v] = kNegInf;
+        for (int v = 0; v < 16; ++v)
+          if (16 * (v >> 3) + (v & 7) >= room) sc[qb][v] = kNegInf;
+      } else {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kblk0 + 16 * (v >> 3) + 8 * h + (v & 7);
+          if (key >= lim[qb]) sc[qb][v] = kNegInf;
+        }
       }
+    }
   };
   auto max_block = [&](f32x16 (&sc)[QB]) {
 #pragma unroll
