@@ -46,7 +46,10 @@
 //
 // K/V tiles of 64 keys (four 16-token pages gathered through the page table)
 // go from HBM straight into LDS (global_load_lds_dwordx4, no registers), four
-// buffers with three tiles in flight.  Waves w and w + 4 fetch page w % 4 of
+// buffers with three tiles in flight.  Long units with token-minor V run a
+// software-pipelined key loop instead (PIPE): the scores of the next 32-key
+// block are formed on the matrix cores while the current block is
+// exponentiated, over five buffers.  Waves w and w + 4 fetch page w % 4 of
 // each tile, half of it each: each load instruction reads 1 KB of one page
 // (a scalar page base plus a fixed lane offset) and fills 1 KB of LDS.  K rows land XOR-swizzled, a
 // token-minor V page ([D][16 keys]) with the two 8-key halves of every other
