@@ -239,37 +239,52 @@ MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_
                  "GRBM_GUI_ACTIVE")
 
 
-def summarize_mfma(pmc_dir, bench_stdout, out_path, command, workload):
-    """Markdown summary of one rocprofv3 --pmc pass of MFMA counters over the
-    attention kernel: the bf16 MFMA work the hardware counted (MOPS, units of
-    512 flops) against the algorithmic FLOPs, and the MFMA-busy share."""
-    rows = [r for r in _counter_rows(pmc_dir) if _kernel_key(r["Kernel_Name"]) == "window_attention"]
+def _by_variant(rows):
+    """Counter averages per dispatch of each kernel variant in the rows
+    (variant -> (dispatches, {counter: average})), in order of appearance."""
     per = {}
     for r in rows:
-        per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-    avg = {k: sum(v) / len(v) for k, v in per.items()}
+        per.setdefault(_variant(r["Kernel_Name"]), {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    out = {}
+    for var, cs in per.items():
+        out[var] = (max(len(v) for v in cs.values()), {k: sum(v) / len(v) for k, v in cs.items()})
+    return out
+
+
+def summarize_mfma(pmc_dir, bench_stdout, out_path, command, workload):
+    """Markdown summary of one rocprofv3 --pmc pass of MFMA counters over the
+    attention kernel, one section per kernel variant the run launched (the
+    timed layout's and the other V layout's): the bf16 MFMA work the hardware
+    counted (MOPS, units of 512 flops) against the algorithmic FLOPs, and the
+    MFMA-busy share."""
+    rows = [r for r in _counter_rows(pmc_dir) if _kernel_key(r["Kernel_Name"]) == "window_attention"]
     line = None
     with open(bench_stdout) as f:
         for ln in f:
             if ln.startswith("{"):
                 line = json.loads(ln)
     gflop = line["attention"]["gflop"] if line else float("nan")
-    counted = avg.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512 / 1e9
-    mfma_insts = avg.get("SQ_INSTS_MFMA", 0.0)
+    timed = line["attention"].get("kernel") if line else None
     lines = ["# window attention: MFMA counters", "", f"Workload {workload}, one rocprofv3 --pmc pass, average per "
-             f"dispatch over {len(rows) // max(1, len(per))} dispatches.", "", "Command:", "", "```", command, "```", "",
-             "| counter | value per dispatch |", "|---|---|"]
-    for k in MFMA_COUNTERS:
-        if k in avg:
-            lines.append(f"| {k} | {avg[k]:.4g} |")
-    lines += ["", f"- bf16 MFMA work counted: {counted:.1f} GFLOP (MOPS x 512) against {gflop:.1f} GFLOP algorithmic "
-              f"(ratio {counted / gflop:.4f}; the extra is the reference block, whose scores are formed twice).",
-              f"- MFMA instructions: {mfma_insts:.4g} (32x32x16 bf16, 32768 flops each: "
-              f"{mfma_insts * 32768 / 1e9:.1f} GFLOP)."]
-    if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and "GRBM_GUI_ACTIVE" in avg:
-        busy = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * 256 * avg["GRBM_GUI_ACTIVE"] / 8)
-        lines.append(f"- MFMA busy share: {100 * busy:.1f}% = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x 256 CUs x "
-                     "GRBM_GUI_ACTIVE / 8), reading GRBM_GUI_ACTIVE as summed over the 8 XCDs.")
+             "dispatch of each kernel variant the run launched.", "", "Command:", "", "```", command, "```"]
+    groups = _by_variant(rows)
+    for var in sorted(groups, key=lambda v: v != timed):
+        n, avg = groups[var]
+        counted = avg.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512 / 1e9
+        mfma_insts = avg.get("SQ_INSTS_MFMA", 0.0)
+        role = "the timed call" if var == timed else "the other V layout"
+        lines += ["", f"## `{var}` ({role}, {n} dispatches)", "", "| counter | value per dispatch |", "|---|---|"]
+        for k in MFMA_COUNTERS:
+            if k in avg:
+                lines.append(f"| {k} | {avg[k]:.4g} |")
+        lines += ["", f"- bf16 MFMA work counted: {counted:.1f} GFLOP (MOPS x 512) against {gflop:.1f} GFLOP algorithmic "
+                  f"(ratio {counted / gflop:.4f}; the extra is the masked keys of each sequence's last 64-key tile).",
+                  f"- MFMA instructions: {mfma_insts:.4g} (32x32x16 bf16, 32768 flops each: "
+                  f"{mfma_insts * 32768 / 1e9:.1f} GFLOP)."]
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and "GRBM_GUI_ACTIVE" in avg:
+            busy = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * 256 * avg["GRBM_GUI_ACTIVE"] / 8)
+            lines.append(f"- MFMA busy share: {100 * busy:.1f}% = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x 256 CUs x "
+                         "GRBM_GUI_ACTIVE / 8), reading GRBM_GUI_ACTIVE as summed over the 8 XCDs.")
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -277,30 +292,29 @@ def summarize_mfma(pmc_dir, bench_stdout, out_path, command, workload):
 
 def summarize_counters(pmc_dir, kernel, out_path, command, workload):
     """Markdown table of one rocprofv3 --pmc pass: each counter's average per
-    dispatch of one kernel (a key of _KERNELS), with the LDS bank-conflict
-    share and the VALU issue share when their counters are there."""
+    dispatch of one kernel (a key of _KERNELS), one section per kernel variant
+    the run launched, with the LDS bank-conflict share and the VALU issue
+    share when their counters are there."""
     rows = [r for r in _counter_rows(pmc_dir) if _kernel_key(r["Kernel_Name"]) == kernel]
-    per = {}
-    for r in rows:
-        per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-    avg = {k: sum(v) / len(v) for k, v in per.items()}
-    n = len(rows) // max(1, len(per))
     lines = [f"# {kernel}: rocprofv3 counters", "", f"Workload {workload}, one rocprofv3 --pmc pass, average per "
-             f"dispatch over {n} dispatches.", "", "Command:", "", "```", command, "```", "",
-             "| counter | value per dispatch |", "|---|---|"]
-    for k in sorted(avg):
-        lines.append(f"| {k} | {avg[k]:.4g} |")
-    lines.append("")
-    if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_LDS_IDX_ACTIVE"):
-        lines.append(f"- LDS bank-conflict cycles per LDS-active cycle: "
-                     f"{avg['SQ_LDS_BANK_CONFLICT'] / avg['SQ_LDS_IDX_ACTIVE']:.2e} "
-                     "(SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE).")
-    if "SQ_ACTIVE_INST_VALU" in avg and avg.get("SQ_WAVE_CYCLES"):
-        lines.append(f"- VALU issue share of wave cycles: {100 * avg['SQ_ACTIVE_INST_VALU'] / avg['SQ_WAVE_CYCLES']:.1f}% "
-                     "(SQ_ACTIVE_INST_VALU / SQ_WAVE_CYCLES).")
-    if "SQ_WAIT_INST_ANY" in avg and avg.get("SQ_WAVE_CYCLES"):
-        lines.append(f"- Waiting for any instruction's inputs: {100 * avg['SQ_WAIT_INST_ANY'] / avg['SQ_WAVE_CYCLES']:.1f}% "
-                     "of wave cycles (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES).")
+             "dispatch of each kernel variant the run launched.", "", "Command:", "", "```", command, "```"]
+    groups = _by_variant(rows)
+    for var in groups:
+        n, avg = groups[var]
+        lines += ["", f"## `{var}` ({n} dispatches)", "", "| counter | value per dispatch |", "|---|---|"]
+        for k in sorted(avg):
+            lines.append(f"| {k} | {avg[k]:.4g} |")
+        lines.append("")
+        if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_LDS_IDX_ACTIVE"):
+            lines.append(f"- LDS bank-conflict cycles per LDS-active cycle: "
+                         f"{avg['SQ_LDS_BANK_CONFLICT'] / avg['SQ_LDS_IDX_ACTIVE']:.2e} "
+                         "(SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE).")
+        if "SQ_ACTIVE_INST_VALU" in avg and avg.get("SQ_WAVE_CYCLES"):
+            lines.append(f"- VALU issue share of wave cycles: {100 * avg['SQ_ACTIVE_INST_VALU'] / avg['SQ_WAVE_CYCLES']:.1f}% "
+                         "(SQ_ACTIVE_INST_VALU / SQ_WAVE_CYCLES).")
+        if "SQ_WAIT_INST_ANY" in avg and avg.get("SQ_WAVE_CYCLES"):
+            lines.append(f"- Waiting for any instruction's inputs: {100 * avg['SQ_WAIT_INST_ANY'] / avg['SQ_WAVE_CYCLES']:.1f}% "
+                         "of wave cycles (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES).")
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
