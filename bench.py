@@ -359,15 +359,29 @@ def summarize_stats(stats_dir, bench_stdout, out_path, command):
                   "| kernel | rocprofv3 trace average (us) | bench.py event average (us) |", "|---|---|---|"]
         ev = {"window_attention": line["attention"]["ms"] * 1e3,
               "edit_select": (line.get("edit_select") or {}).get("ms", 0) * 1e3}
-        by = {}
+        # the timed attention variant only: the other V layout's calls come
+        # after the timed steps and are reported on their own line
+        timed_var = line["attention"].get("kernel")
+        by, other = {}, {}
         for r in sorted(trace, key=lambda r: int(r["Start_Timestamp"])):
             k = _kernel_key(r["Kernel_Name"])
-            if k:
-                by.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+            if not k:
+                continue
+            d_us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            var = _variant(r["Kernel_Name"])
+            if k == "window_attention" and timed_var and var != timed_var:
+                other.setdefault(var, []).append(d_us)
+            else:
+                by.setdefault(k, []).append(d_us)
         for k, d in sorted(by.items()):
             d = d[-steps:]
-            lines.append(f"| {k} | {sum(d) / len(d):.2f} | {ev[k]:.2f} |" if k in ev else
-                         f"| {k} | {sum(d) / len(d):.2f} | (part of a call timed as a whole) |")
+            name = f"{k} (`{timed_var}`)" if k == "window_attention" and timed_var else k
+            lines.append(f"| {name} | {sum(d) / len(d):.2f} | {ev[k]:.2f} |" if k in ev else
+                         f"| {name} | {sum(d) / len(d):.2f} | (part of a call timed as a whole) |")
+        for var, d in other.items():
+            ov = (line.get("attention_other_v_layout") or {})
+            ev_o = f"{ov['ms'] * 1e3:.2f}" if ov.get("kernel") == var and "ms" in ov else "—"
+            lines.append(f"| window_attention, other V layout (`{var}`, {len(d)} calls) | {sum(d) / len(d):.2f} | {ev_o} |")
         if "window_attention_merge" in by and "window_attention" in by:
             a, m = by["window_attention"][-steps:], by["window_attention_merge"][-steps:]
             lines += ["", f"The attention call is the main kernel plus the split merge: "
