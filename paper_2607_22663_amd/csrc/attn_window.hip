@@ -705,7 +705,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // issues tile t + 4 into the buffer of tile t - 1, which every wave
   // finished reading before the barrier that ended step t - 1, and its own
   // barrier lands tile t + 2.  Every LDS read of step t is of tile t or t + 1.
-    // numerators of one block to bf16 P^T (keys 16m + 8h .. +7), row sums of
+  //
+  // numerators of one block to bf16 P^T (keys 16m + 8h .. +7), row sums of
   // the bf16 numerators
   auto softmax_blk = [&](const f32x16 (&s)[QB], bf16x8 (&pb)[2]) {
     const float msafe = (m_ref[0] == kNegInf) ? 0.f : m_ref[0];
