@@ -154,14 +154,29 @@ __device__ __forceinline__ bf16x4 lds_read_tr4(const char *at) {
 
 typedef const __attribute__((address_space(4))) int32_t const_i32;
 
+// A load that stays where it is written: the compiler would otherwise move a
+// plain load into the branch that uses it, behind an earlier branch's wait,
+// so that loads meant to be in flight together are issued one after another.
+// (A relaxed atomic load is never moved; at workgroup scope it is an ordinary
+// vector load.)
+__device__ __forceinline__ int32_t load_now(const int32_t *ptr) {
+  return __hip_atomic_load(ptr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // Page id of page `wv` (0..3) of the 64-key tile starting at key0, read with a scalar
-// load (the page table is constant during the kernel).  Slots past the table
-// row are clamped into it and ids into the pool; such pages only feed keys
-// that are masked and whose V rows are zeroed.
-__device__ __forceinline__ int wave_page(const AttnParams &p, int b, int key0, int wv) {
-  const_i32 *row = (const_i32 *)(p.page_table) + static_cast<int64_t>(b) * p.max_pages;
+// load (the page table is constant during the kernel), or with load_now when
+// kNow (the first tile's, read together with the lengths).  Slots past the
+// table row are clamped into it and ids into the pool; such pages only feed
+// keys that are masked and whose V rows are zeroed.
+template <bool kNow = false>
+__device__ __forceinline__ int wave_page(const AttnParams &p, int b, int key0, int wv,
+                                         std::integral_constant<bool, kNow> = {}) {
+  const int64_t row = static_cast<int64_t>(b) * p.max_pages;
   const int slot = min(key0 / kPageSize + wv, p.max_pages - 1);
-  return min(max(row[slot], 0), p.num_pages - 1);
+  int pid;
+  if constexpr (kNow) pid = __builtin_amdgcn_readfirstlane(load_now(p.page_table + row + slot));
+  else pid = ((const_i32 *)(p.page_table))[row + slot];
+  return min(max(pid, 0), p.num_pages - 1);
 }
 
 // Per-lane byte offsets, within one K page, of the chunks that the direct
@@ -312,7 +327,9 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   // later splits (later splits of short sequences have no work).  Either way
   // the qtiles query tiles of a group, which read the same keys, take
   // consecutive slots of one XCD so that the second finds the keys in its L2.
-  if (p.gate && *p.gate == 0) return;     // gated off: the call does nothing
+  // gated off: the call does nothing (the gate is read together with the
+  // work unit and checked once both are in)
+  const int32_t gate = load_now(p.gate ? p.gate : p.prefix_lens);
   const int64_t id = blockIdx.x;
   int64_t grp;
   int qtile;
@@ -333,6 +350,7 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int rank = static_cast<int>(rg / p.num_kv_heads);
   const int g = static_cast<int>(rg % p.num_kv_heads);
   const int b = (p.order_kind == kOrderSeqs && rank < p.order_n) ? p.order[rank] : rank;
+  if (p.gate && gate == 0) return;
 
   const int G = p.group;
   const int tid = threadIdx.x;
@@ -367,14 +385,17 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   const int wpart = wv / 4;                                  // and which part of it
   const int kb = split * p.kv_chunk;
 
-  // The reads below depend only on b and are issued together: the lengths
-  // and the page of the first tile that this wave loads.  With a fixed
+  // The reads below depend only on b and are issued together: the lengths,
+  // the page of the first tile that this wave loads and, in lane j, the
+  // window length of sequence j < b (the first 64 of those).  With a fixed
   // window, window_lens may be absent and prefix_lens is read in its place
   // and ignored.
   const bool fixed = p.fixed_window >= 0;
-  const int32_t P_dev = p.prefix_lens[b];
-  const int32_t W_dev = (fixed ? p.prefix_lens : p.window_lens)[b];
-  const int pid0 = wave_page(p, b, kb, wpage);
+  const int32_t *wl = fixed ? p.prefix_lens : p.window_lens;
+  const int32_t P_dev = load_now(p.prefix_lens + b);
+  const int32_t W_dev = load_now(wl + b);
+  const int32_t wl_lane = load_now(wl + min(lane, b));
+  const int pid0 = wave_page(p, b, kb, wpage, std::true_type{});
   // lengths are clamped to the host-validated bounds, so a wrong device value
   // can give wrong numbers but never an access outside q, out or the workspace
   const int W = fixed ? p.fixed_window : min(max(W_dev, 0), p.max_window);
@@ -392,7 +413,8 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
   if (fixed) {
     cu = b * p.fixed_window;
   } else {
-    for (int j = lane; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
+    cu = lane < b ? min(max(wl_lane, 0), p.max_window) : 0;
+    for (int j = lane + 64; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
     cu = __builtin_amdgcn_readfirstlane(cu);   // the same in every lane
@@ -1038,10 +1060,21 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
 //   M = max m_s,  O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s   (split order).
 template <int D>
 __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams p) {
-  if (p.gate && *p.gate == 0) return;
+  // The gate, the lengths of b and, in lane j, the window length of sequence
+  // j < b (the first 64 of those) are requested together; the partial sums
+  // follow once the split count is known.  With a fixed window, window_lens
+  // may be absent and prefix_lens is read in its place and ignored.
   const int b = blockIdx.y;
-  const int P = min(max(p.prefix_lens[b], 0), p.max_prefix);
-  const int W = p.fixed_window >= 0 ? p.fixed_window : min(max(p.window_lens[b], 0), p.max_window);
+  const int lane = threadIdx.x & 63;
+  const bool fixed = p.fixed_window >= 0;
+  const int32_t *wl = fixed ? p.prefix_lens : p.window_lens;
+  const int32_t gate = load_now(p.gate ? p.gate : p.prefix_lens);
+  const int32_t P_dev = load_now(p.prefix_lens + b);
+  const int32_t W_dev = load_now(wl + b);
+  const int32_t wl_lane = load_now(wl + min(lane, b));
+  if (p.gate && gate == 0) return;
+  const int P = min(max(P_dev, 0), p.max_prefix);
+  const int W = fixed ? p.fixed_window : min(max(W_dev, 0), p.max_window);
   const int n_all = P + W;
   const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
   if (nsplit == 1) return;                  // written directly by the main kernel
@@ -1051,10 +1084,11 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   // first query row of sequence b: the window lengths before it, summed
   // across the lanes of the wave (before any lane leaves)
   int cu = 0;
-  if (p.fixed_window >= 0) {
+  if (fixed) {
     cu = b * p.fixed_window;
   } else {
-    for (int j = threadIdx.x & 63; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
+    cu = lane < b ? min(max(wl_lane, 0), p.max_window) : 0;
+    for (int j = lane + 64; j < b; j += 64) cu += min(max(p.window_lens[j], 0), p.max_window);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
   }
