@@ -1121,6 +1121,9 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
       ml[j] = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
       po[j] = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
     }
+    // every load of the chunk is issued before any is used (the scheduler
+    // would otherwise interleave them with the sums to save registers)
+    __builtin_amdgcn_sched_barrier(0);
     float cmax = mrun;
 #pragma unroll
     for (int j = 0; j < C; ++j)
