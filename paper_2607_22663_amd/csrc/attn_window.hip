@@ -365,7 +365,10 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
     if constexpr (!PIPE) {
       return __syncthreads_or(v) != 0;
     } else {
-      volatile int *slot = reinterpret_cast<volatile int *>(lds4);
+      // (an LDS-typed pointer: a generic one made the compiler keep a 64-bit
+      // address per word live across the key loop, and spill them)
+      typedef __attribute__((address_space(3))) volatile int lds_word;
+      lds_word *slot = (lds_word *)(lds4);
       const bool w = __builtin_amdgcn_ballot_w64(v) != 0;
       lds_barrier();       // earlier reads of the words are done
       if ((tid & 63) == 0) slot[wave] = w;
