@@ -431,6 +431,29 @@ def _time_cold(fn, n, flush):
     return float(np.mean(d)), float(np.median(d))
 
 
+def _time_cold_pair(fa, fb, n, flush):
+    """_time_cold of two calls taken in turn (a, b, a, b, ...), so that both
+    run under the same clock and power state; returns ((mean, median) of a,
+    (mean, median) of b)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        fa()
+        fb()
+    torch.cuda.synchronize()
+    d = ([], [])
+    for _ in range(n):
+        for fn, out in ((fa, d[0]), (fb, d[1])):
+            flush.view(torch.float32).sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1) / 1e3)
+    return tuple((float(np.mean(x)), float(np.median(x))) for x in d)
+
+
 def _host_issue_time(fn, n):
     """Host time to issue one call of fn (mean over n calls queued behind a
     GPU spin, so that the queue never waits on the GPU), synchronised after."""
@@ -794,11 +817,14 @@ def bench_other_workloads(mbe, headline, steps):
             flops, nbytes = attention_work(case)
             roof = min(PEAK_BF16_TFLOPS, flops / nbytes * PEAK_HBM_GBS / 1e3)
             r = {}
-            for vt, vpages in ((False, c.v_pages), (True, c.v_pages.transpose(2, 3).contiguous())):
-                t, tm = timed(lambda: mbe.window_attention(
-                    c.q, c.k_pages, vpages, c.page_table, c.prefix_lens, c.window_lens, case.block_size, out=out,
-                    max_prefix_len=mp, max_window_len=mw, host_prefix_lens=case.prefix_lens,
-                    host_window_lens=case.window_lens))
+            # both V layouts, their calls taken in turn
+            layouts = ((False, c.v_pages), (True, c.v_pages.transpose(2, 3).contiguous()))
+            calls = [lambda vp=vp: mbe.window_attention(
+                c.q, c.k_pages, vp, c.page_table, c.prefix_lens, c.window_lens, case.block_size, out=out,
+                max_prefix_len=mp, max_window_len=mw, host_prefix_lens=case.prefix_lens,
+                host_window_lens=case.window_lens) for _, vp in layouts]
+            times = _time_cold_pair(calls[0], calls[1], steps, flush)
+            for (vt, _), (t, tm) in zip(layouts, times):
                 tf = flops / t / 1e12
                 r["attention" if not vt else "attention_v_token_major"] = {
                     "ms": round(t * 1e3, 4), "ms_median": round(tm * 1e3, 4), "tflops": round(tf, 2),
@@ -806,7 +832,7 @@ def bench_other_workloads(mbe, headline, steps):
                     "roofline_tflops": round(roof, 1), "pct_of_roofline": round(100 * tf / roof, 2),
                     "gbs": round(nbytes / t / 1e9, 1),
                     "roofline": attention_roofline(flops, nbytes, t, attention_kernel_name(case, 0, vt))}
-                del vpages
+            del layouts, calls
             del c, out
             if wl.edit is not None and k is None:
                 ec = synth.workload_edit(name)
