@@ -83,3 +83,28 @@ def test_batch_beyond_dispatch_order_table(gpu):
     ref = oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
                                   case.window_lens, 16)
     assert_attn_close(out.cpu(), ref, "1100 sequences")
+
+
+@pytest.mark.parametrize("mode", ["bidir", "block_causal"])
+def test_many_sequences_split_merge(gpu, mode):
+    """80 sequences with ragged windows and forced splits.  The main kernel and
+    the split merge find a sequence's first query row by summing the window
+    lengths of the sequences before it, 64 lanes at a time, so sequences past
+    the 64th take a second round of that sum in both kernels."""
+    rng = np.random.default_rng(91)
+    n = 80
+    spec = synth.AttnSpec(n, 16, 2, ("fixed", 0), 4, 2, 64)
+    P = [int(x) for x in rng.integers(100, 700, size=n)]
+    W = [int(x) * 16 for x in rng.integers(0, 3, size=n)]
+    W[-1] = 32
+    case = synth.make_attention_case(spec, 92, prefix_lens=P, window_lens=W, tail_fill=float("nan"))
+    c = case.to(DEV)
+    say(f"  80 sequences, {mode}, split 128")
+    out = gpu.window_attention(c.q, c.k_pages, c.v_pages, c.page_table, c.prefix_lens, c.window_lens, 16,
+                               mask_mode=mode, kv_split_tokens=128, host_prefix_lens=case.prefix_lens,
+                               host_window_lens=case.window_lens)
+    torch.cuda.synchronize()
+    m = oracle.MASK_BIDIR if mode == "bidir" else oracle.MASK_BLOCK_CAUSAL
+    ref = oracle.window_attention(case.q, case.k_pages, case.v_pages, case.page_table, case.prefix_lens,
+                                  case.window_lens, 16, m)
+    assert_attn_close(out.cpu(), ref, f"80 sequences {mode}")
