@@ -1059,8 +1059,9 @@ __global__ __launch_bounds__(kT, 1) void window_attention_kernel(AttnParams p) {
 // Split-KV merge, run after the main kernel when some sequence was split (the
 // kernel boundary makes every partial result visible; no cross-workgroup
 // fences inside the main kernel).  Block (x, b) merges items x*256 .. of
-// sequence b, an item being 4 dims of one (window row, query head):
+// sequence b, an item being kMergeDims dims of one (window row, query head):
 //   M = max m_s,  O = sum 2^(m_s-M) O_s / sum 2^(m_s-M) l_s   (split order).
+constexpr int kMergeDims = 8;   // dims per merge thread: two 16-byte loads per split, one 16-byte store
 template <int D>
 __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams p) {
   // The gate, the lengths of b and, in lane j, the window length of sequence
@@ -1081,8 +1082,8 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   const int n_all = P + W;
   const int nsplit = min(p.splits, max(1, (n_all + p.kv_chunk - 1) / p.kv_chunk));
   if (nsplit == 1) return;                  // written directly by the main kernel
-  constexpr int D4 = D / 4;
-  const int64_t items = static_cast<int64_t>(W) * p.num_q_heads * D4;
+  constexpr int DI = D / kMergeDims;
+  const int64_t items = static_cast<int64_t>(W) * p.num_q_heads * DI;
   const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   // first query row of sequence b: the window lengths before it, summed
   // across the lanes of the wave (before any lane leaves)
@@ -1096,8 +1097,8 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
     for (int o = 32; o >= 1; o >>= 1) cu += __shfl_xor(cu, o);
   }
   if (item >= items) return;
-  const int64_t r = item / D4;              // (window row, query head) within the sequence
-  const int d0 = static_cast<int>(item % D4) * 4;
+  const int64_t r = item / DI;              // (window row, query head) within the sequence
+  const int d0 = static_cast<int>(item % DI) * kMergeDims;
   if (cu + r / p.num_q_heads >= p.total_q) return;
   if (p.block_flags &&
       !p.block_flags[static_cast<int64_t>(b) * p.flag_stride + (r / p.num_q_heads) / p.block_size])
@@ -1105,24 +1106,28 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
   const int64_t rowidx = static_cast<int64_t>(cu) * p.num_q_heads + r;
   const int64_t split_stride = static_cast<int64_t>(p.total_q) * p.num_q_heads;
   // Every split below nsplit wrote this row (zeros and a -inf reference when
-  // it saw none of its keys).  Splits are read in chunks of C = 16, 8, 4, 2
-  // or 1 (the smallest that holds what is left, at most 16), all loads of a
+  // it saw none of its keys).  Splits are read in chunks of C = 8, 4, 2 or 1
+  // (the smallest that holds what is left, at most 8; chunks of 16 would hold
+  // twice the registers and halve the waves a SIMD keeps), all loads of a
   // chunk issued together (past nsplit the last split is read again and
   // weighted 0); the running maximum M and the sums are rescaled when a chunk
-  // raises M.  With at most 16 splits this is exactly the two-step form
+  // raises M.  With at most 8 splits this is exactly the two-step form
   // (M first, then the sums in split order).
   float mrun = kNegInf, lsum = 0.f;
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  constexpr int Q = kMergeDims / 4;         // 16-byte loads per split
+  float o[kMergeDims] = {};
   auto chunk = [&](int s0, auto csize) {
     constexpr int C = decltype(csize)::value;
     const int n = min(C, nsplit - s0);
     float2 ml[C];
-    float4 po[C];
+    float4 po[C][Q];
 #pragma unroll
     for (int j = 0; j < C; ++j) {
       const int64_t sp = s0 + min(j, n - 1);
       ml[j] = *reinterpret_cast<const float2 *>(p.part_ml + (sp * split_stride + rowidx) * 2);
-      po[j] = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0);
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        po[j][q] = *reinterpret_cast<const float4 *>(p.part_o + (sp * split_stride + rowidx) * D + d0 + 4 * q);
     }
     // every load of the chunk is issued before any is used (the scheduler
     // would otherwise interleave them with the sums to save registers)
@@ -1134,34 +1139,36 @@ __global__ __launch_bounds__(256) void window_attention_merge_kernel(AttnParams 
     // old sums to the new maximum (nothing to rescale while M is -inf)
     const float rescale = mrun == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mrun - cmax);
     lsum *= rescale;
-    o.x *= rescale;
-    o.y *= rescale;
-    o.z *= rescale;
-    o.w *= rescale;
+#pragma unroll
+    for (int i = 0; i < kMergeDims; ++i) o[i] *= rescale;
 #pragma unroll
     for (int j = 0; j < C; ++j) {
       const float wgt = (j < n && ml[j].x != kNegInf) ? __builtin_amdgcn_exp2f(ml[j].x - cmax) : 0.f;
       lsum += wgt * ml[j].y;
-      o.x += wgt * po[j].x;
-      o.y += wgt * po[j].y;
-      o.z += wgt * po[j].z;
-      o.w += wgt * po[j].w;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        o[4 * q + 0] += wgt * po[j][q].x;
+        o[4 * q + 1] += wgt * po[j][q].y;
+        o[4 * q + 2] += wgt * po[j][q].z;
+        o[4 * q + 3] += wgt * po[j][q].w;
+      }
     }
     mrun = cmax;
   };
   for (int s0 = 0; s0 < nsplit;) {
     const int left = nsplit - s0;
-    if (left > 8) { chunk(s0, std::integral_constant<int, 16>{}); s0 += 16; }
-    else if (left > 4) { chunk(s0, std::integral_constant<int, 8>{}); s0 += 8; }
+    if (left > 4) { chunk(s0, std::integral_constant<int, 8>{}); s0 += 8; }
     else if (left > 2) { chunk(s0, std::integral_constant<int, 4>{}); s0 += 4; }
     else if (left == 2) { chunk(s0, std::integral_constant<int, 2>{}); s0 += 2; }
     else { chunk(s0, std::integral_constant<int, 1>{}); s0 += 1; }
   }
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-  uint2 st;
-  st.x = pack_bf16x2(o.x * inv, o.y * inv);
-  st.y = pack_bf16x2(o.z * inv, o.w * inv);
-  *reinterpret_cast<uint2 *>(p.out + rowidx * D + d0) = st;
+  uint4 st;
+  st.x = pack_bf16x2(o[0] * inv, o[1] * inv);
+  st.y = pack_bf16x2(o[2] * inv, o[3] * inv);
+  st.z = pack_bf16x2(o[4] * inv, o[5] * inv);
+  st.w = pack_bf16x2(o[6] * inv, o[7] * inv);
+  *reinterpret_cast<uint4 *>(p.out + rowidx * D + d0) = st;
 }
 
 template <int D, int MODE>
@@ -1178,7 +1185,7 @@ hipError_t launch_t(const AttnParams &p, hipStream_t stream) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits == 1) return e;
-  const int64_t items = static_cast<int64_t>(p.max_window) * p.num_q_heads * (D / 4);
+  const int64_t items = static_cast<int64_t>(p.max_window) * p.num_q_heads * (D / kMergeDims);
   const dim3 mgrid(static_cast<unsigned>((items + 255) / 256), static_cast<unsigned>(p.batch));
   hipLaunchKernelGGL((window_attention_merge_kernel<D>), mgrid, dim3(256), 0, stream, p);
   return hipGetLastError();
