@@ -61,10 +61,10 @@ def test_forced_split_kv(gpu, split, vt):
 
 @pytest.mark.parametrize("nsplit", [2, 3, 5, 8, 9, 16, 17, 32, 33, 40])
 def test_merge_chunk_boundaries(gpu, nsplit):
+    """Split counts on both sides of the merge's chunk sizes (8, 4, 2, 1) and
+    of several chunks: a 64-key split over P + W = 64 * nsplit - 8 keys, with
+    a ragged second sequence of fewer splits and one whose window is empty."""
     vt = nsplit % 2 == 1            # both V layouts over the split counts
-    """Split counts on both sides of the merge's chunk sizes (16, 8, 4, 2, 1):
-    a 64-key split over P + W = 64 * nsplit - 8 keys, with a ragged second
-    sequence of fewer splits and one whose window is empty."""
     spec = synth.AttnSpec(3, 16, 2, ("fixed", 0), 8, 2, 64)
     P0 = 64 * nsplit - 8 - 32
     case = synth.make_attention_case(spec, 90 + nsplit, prefix_lens=[P0, max(0, P0 // 3), 100],
